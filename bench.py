@@ -1,0 +1,221 @@
+"""Benchmark: DFloat11 block decompression on one MI355X.
+
+One step = decode one Llama-3-8B-shaped transformer block (q, k, v, o, gate,
+up, down concatenated: 218,103,808 BF16 weights) from its DFloat11 stream,
+resident in HBM, into a reused BF16 workspace -- the whole decode path in
+one launch.  Prints one JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                  [--no-cpu-baseline] [--calib] [--cold]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decompressed BF16 GB/s per block and % of HBM roofline (bit-exact)"
+HBM_PEAK_GBS = 8000.0
+
+
+def workload(name: str):
+    from paper_2504_11651_amd import synth
+    if name == "llama3_8b_block":
+        return synth.llama3_8b_block()[0]
+    if name == "heavy_tailed_block":
+        return synth.heavy_tailed_block()
+    if name == "llama31_70b_block":
+        return synth.llama31_70b_block()[0]
+    if name == "matrix_4096":
+        return synth.matrix_4096()
+    raise SystemExit(f"unknown workload {name}")
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(hs, w, min_seconds: float = 10.0, max_reps: int = 4) -> dict:
+    """The oracle's bit-serial decode of the same stream on one host core."""
+    import oracle
+    n = w.size
+    reps, t = 0, 0.0
+    while reps < max_reps and (t < min_seconds or reps == 0):
+        t0 = time.perf_counter()
+        out = oracle.decode_serial(hs.exp, int(hs.sizes.total_bits), hs.sm, n,
+                                   hs.codebook.lengths)
+        t += time.perf_counter() - t0
+        reps += 1
+        assert np.array_equal(out, w), "oracle decode differs from the input"
+    return {"value": round(2.0 * n * reps / t / 1e9, 4), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"whole block stream decoded {reps}x by the oracle's bit-serial tree walk "
+                      f"({n} weights each, {t:.1f} s, 1 thread of {os.cpu_count()} on "
+                      f"{cpu_model()})",
+            "weights_per_s": round(n * reps / t, 1)}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama3_8b_block")
+    ap.add_argument("--threads", type=int, default=None, help="threads per block T")
+    ap.add_argument("--lut-bits", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib", action="store_true",
+                    help="also run a plain device copy of known size (PMC calibration)")
+    ap.add_argument("--cold", action="store_true",
+                    help="also time steps with the 256 MB last-level cache flushed before each")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: the decode is local to each GPU's own streams, "
+              "so runs with more than one GPU are not part of this benchmark", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2504_11651_amd import codec
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    t0 = time.perf_counter()
+    w = workload(args.workload)
+    t_gen = time.perf_counter() - t0
+    lay = codec.make_layout(8, args.threads, args.lut_bits)
+    t0 = time.perf_counter()
+    hs = codec.encode(w, layout=lay)
+    t_enc = time.perf_counter() - t0
+    assert codec.validate(hs) == 0
+    ds = codec.to_device(hs, dev)
+    n = w.size
+    out = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    ref = torch.from_numpy(w.view(np.int16)).to(dev)
+    stream = torch.cuda.current_stream(dev)
+
+    # bit-exact before timing
+    codec.decode_block(ds, out)
+    torch.cuda.synchronize()
+    bit_exact = bool(torch.equal(out.view(torch.int16), ref))
+    assert bit_exact, "decode is not bit-exact"
+    del ref
+
+    for _ in range(args.warmup):
+        codec.decode_block(ds, out)
+    torch.cuda.synchronize()
+
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        starts[i].record(stream)
+        codec.decode_block(ds, out)
+        ends[i].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = np.array([s.elapsed_time(e) for s, e in zip(starts, ends)])
+
+    cold = None
+    if args.cold:
+        scratch = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        cms = []
+        for i in range(max(5, args.steps // 5)):
+            scratch.fill_(i & 0xFF)  # evicts the MALL and L2 (1 GiB written)
+            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s.record(stream)
+            codec.decode_block(ds, out)
+            e.record(stream)
+            torch.cuda.synchronize()
+            cms.append(s.elapsed_time(e))
+        del scratch
+        cold = float(np.median(cms))
+
+    if args.calib:
+        # plain copy kernel of known size for scaling FETCH_SIZE / WRITE_SIZE counters
+        src = torch.empty(1 << 29, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
+    z = hs.sizes
+    exp_bytes_exact = (int(z.total_bits) + 7) // 8
+    read_bytes = exp_bytes_exact + int(z.sm_bytes) + int(z.gap_bytes) + int(z.block_pos_bytes) + \
+        int(z.table_bytes)
+    write_bytes = 2 * n
+    algo_bytes = read_bytes + write_bytes
+    kern_ms = float(ev_ms.mean())
+    achieved = algo_bytes / (kern_ms * 1e-3) / 1e9
+    ms_per_step = wall * 1e3 / args.steps
+    value = 2.0 * n / (ms_per_step * 1e-3) / 1e9
+    grid, block, lds = codec.launch_shape(ds)
+
+    rec = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload,
+            "weights": n,
+            "matrices": "q,k,v,o,gate,up,down (row-major, concatenated into one stream)",
+            "layout": {"bytes_per_thread": int(lay.bytes_per_thread),
+                       "threads_per_block": int(lay.threads_per_block),
+                       "lut_bits": int(lay.lut_bits)},
+            "launch": {"grid": grid, "block": block, "lds_bytes": lds},
+        },
+        "roofline": {
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None,
+        },
+        "pct_hbm_roofline": round(100.0 * achieved / HBM_PEAK_GBS, 2),
+        "weights_per_s": round(n / (ms_per_step * 1e-3), 1),
+        "bit_exact": bit_exact,
+        "kernel_ms": {"mean": round(kern_ms, 5), "median": round(float(np.median(ev_ms)), 5),
+                      "min": round(float(ev_ms.min()), 5), "max": round(float(ev_ms.max()), 5)},
+        "bytes_per_step": {"read": read_bytes, "write": write_bytes, "algorithmic": algo_bytes},
+        "compression": {"bits_per_weight": round(8 + z.total_bits / n, 4),
+                        "ratio": round((read_bytes) / (2.0 * n), 4),
+                        "max_code_len": int(z.max_code_len)},
+        "host_s": {"generate": round(t_gen, 2), "encode": round(t_enc, 2)},
+    }
+    if cold is not None:
+        rec["cold_cache_kernel_ms_median"] = round(cold, 5)
+        rec["cold_cache_bf16_gbs"] = round(2.0 * n / (cold * 1e-3) / 1e9, 2)
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(hs, w)
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

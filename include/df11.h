@@ -1,0 +1,164 @@
+/*
+ * df11.h -- C ABI of the DFloat11 codec for MI355X (gfx950).
+ *
+ * DFloat11 (arXiv 2504.11651) stores a BF16 tensor losslessly as
+ *   - EncodedExponent:    the 8-bit exponents, Huffman coded and tightly
+ *                         bit-packed (Sec. 2.3);
+ *   - PackedSignMantissa: one raw byte per weight, sign in bit 7 and the 7
+ *                         mantissa bits in bits 6..0 (Sec. 2.3, Algorithm 1);
+ *   - Gaps:               per n-byte chunk of EncodedExponent, the bit offset
+ *                         of the first code that starts in it, 5 bits each
+ *                         (Sec. 2.3.2);
+ *   - BlockOutputPos:     per block of T chunks, the index of its first output
+ *                         element (Sec. 2.3.2, Algorithm 1);
+ *   - decode tables:      the code book in table form (Sec. 2.3.1).
+ * Decompression (Algorithm 1) turns these back into bit-identical BF16.
+ *
+ * Byte-level format (every reading of the paper is listed here):
+ *   - stream bit k is bit 7-(k%8) of byte k/8 (first code bit = most
+ *     significant); codes are canonical, ordered by (length, exponent value);
+ *     total_bits = sum of the code lengths; the stream is zero padded to
+ *     exp_bytes = B*n*T + 16 bytes;
+ *   - chunk c covers stream bits [8n*c, 8n*(c+1)); C = ceil(total_bits/8n)
+ *     chunks; B = ceil(C/T) blocks;
+ *   - Gaps[c] = (first code start >= 8n*c, the end of the stream counting as
+ *     a start) - 8n*c, for c = 0 .. B*T (B*T+1 slots); 0 for a chunk past the
+ *     end; slot c occupies packed bits [5c, 5c+5), most significant first, in
+ *     gap_bytes = 4*(ceil(5*(B*T+1)/32)+2) bytes;
+ *   - BlockOutputPos[b] = number of codes starting before bit 8n*T*b, for
+ *     b = 0 .. B (B+1 entries; the last is n_elems);
+ *   - all 256 exponent values are codable (the paper's format reserves
+ *     240..255 as table pointers; this one does not need to);
+ *   - code lengths are capped at max_code_len <= 32 (gaps fit 5 bits); when
+ *     plain Huffman is deeper, optimal capped lengths come from package-merge.
+ *   - the decode-table blob (table_bytes) is this library's own layout,
+ *     built from the code book by df11_build_tables; it is opaque to callers.
+ *
+ * Memory ownership: the caller allocates and frees every buffer.  Host
+ * functions take host pointers; df11_decode_block takes device pointers
+ * (inside df11_stream) and a device output pointer.  The library keeps no
+ * per-call state and allocates no device memory on the decode path.
+ *
+ * Errors: every function returns DF11_OK (0) or a negative DF11_E_* code;
+ * nothing is thrown across the ABI.  df11_strerror names a code.
+ */
+#ifndef DF11_H
+#define DF11_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DF11_OK 0
+#define DF11_E_INVALID_ARG (-1)       /* null pointer, bad size, bad layout */
+#define DF11_E_CAP_INFEASIBLE (-2)    /* 2^max_code_len < number of symbols */
+#define DF11_E_BUFFER_TOO_SMALL (-3)  /* an output capacity is too small */
+#define DF11_E_CORRUPT (-4)           /* df11_validate found an inconsistency */
+#define DF11_E_HIP (-5)               /* HIP runtime or launch failure */
+#define DF11_E_UNSUPPORTED (-6)       /* layout the decoder was not built for */
+
+/* Code book: histogram of the exponents, canonical code per exponent. */
+typedef struct {
+    uint32_t max_code_len; /* longest code in use (0 when no symbol is used) */
+    uint32_t num_symbols;  /* exponent values with a non-zero count */
+    uint64_t count[256];   /* histogram of exponent values */
+    uint8_t len[256];      /* code length in bits, 0 = value not used */
+    uint32_t code[256];    /* canonical code, right aligned in len bits */
+} df11_codebook;
+
+/* Work partition of the stream (Sec. 2.3.2). */
+typedef struct {
+    uint32_t bytes_per_thread;  /* n: bytes of EncodedExponent per thread (decoder: 8) */
+    uint32_t threads_per_block; /* T: threads per block, a multiple of 64, <= 1024 */
+    uint32_t lut_bits;          /* width of the first-level decode table index, 8..12 */
+} df11_layout;
+
+/* Sizes of one encoded stream. */
+typedef struct {
+    uint64_t n_elems;             /* BF16 weights */
+    uint64_t total_bits;          /* sum of code lengths */
+    uint64_t num_chunks;          /* C */
+    uint64_t num_blocks;          /* B */
+    uint64_t exp_bytes;           /* EncodedExponent bytes incl. padding */
+    uint64_t sm_bytes;            /* PackedSignMantissa bytes (= n_elems) */
+    uint64_t gap_bytes;           /* packed Gaps bytes */
+    uint64_t block_pos_bytes;     /* 4 * (B + 1) */
+    uint64_t table_bytes;         /* decode-table blob bytes */
+    uint32_t max_elems_per_block; /* max of BlockOutputPos[b+1]-BlockOutputPos[b]; set by df11_encode */
+    uint32_t max_code_len;        /* longest code in the book */
+} df11_sizes;
+
+/* One encoded stream.  For df11_decode_block the pointers are device
+ * pointers; for df11_validate they are host pointers. */
+typedef struct {
+    const uint8_t *exp;        /* EncodedExponent, sizes.exp_bytes */
+    const uint8_t *sm;         /* PackedSignMantissa, sizes.sm_bytes */
+    const uint8_t *gaps;       /* packed Gaps, sizes.gap_bytes */
+    const uint32_t *block_pos; /* BlockOutputPos, B + 1 entries */
+    const uint8_t *tables;     /* decode-table blob, sizes.table_bytes */
+    df11_sizes sizes;
+    df11_layout layout;
+} df11_stream;
+
+/* Histogram of the exponents of n BF16 weights (bit patterns), optimal code
+ * lengths capped at max_code_len (1..32), canonical codes (Sec. 2.3; the
+ * Huffman tree of Sec. 2.1; cap: Sec. 2.3.2).  Host.  Ties between equal
+ * weights are broken leaf first, then by exponent value, then by creation
+ * order, so the result is deterministic. */
+int df11_build_codebook(const uint16_t *bf16, uint64_t n, uint32_t max_code_len,
+                        df11_codebook *out);
+
+/* Same, from a given histogram (no weights needed).  Host. */
+int df11_codebook_from_counts(const uint64_t counts[256], uint32_t max_code_len,
+                              df11_codebook *out);
+
+/* Buffer sizes for encoding the weights counted in cb with layout lay.
+ * max_elems_per_block is left 0 (it depends on the data).  Host. */
+int df11_encoded_sizes(const df11_codebook *cb, const df11_layout *lay, df11_sizes *out);
+
+/* Encode n weights (Sec. 2.3): writes EncodedExponent (exp, zero padded),
+ * PackedSignMantissa (sm), packed Gaps and BlockOutputPos (Sec. 2.3.2).
+ * Each *_cap is the capacity of the buffer in bytes.  The weights must match
+ * the histogram in cb.  Fills *out (including max_elems_per_block).  Host,
+ * multi-threaded. */
+int df11_encode(const uint16_t *bf16, uint64_t n, const df11_codebook *cb, const df11_layout *lay,
+                uint8_t *exp, uint64_t exp_cap, uint8_t *sm, uint64_t sm_cap, uint8_t *gaps,
+                uint64_t gap_cap, uint32_t *block_pos, uint64_t block_pos_cap, df11_sizes *out);
+
+/* Decode-table blob for cb with a lut_bits-wide first-level table
+ * (Sec. 2.3.1 and the appendix on lookup-table decoding).  Host. */
+int df11_build_tables(const df11_codebook *cb, uint32_t lut_bits, uint8_t *tables,
+                      uint64_t table_cap);
+
+/* Consistency check of a stream held in HOST memory: sizes agree with the
+ * layout, Gaps < max_code_len, BlockOutputPos starts at 0, never decreases,
+ * ends at n_elems, and agrees with max_elems_per_block, the table blob is
+ * well formed.  Returns DF11_E_CORRUPT on the first violation.  Host. */
+int df11_validate(const df11_stream *host_view);
+
+/* Decompress one stream into n_elems BF16 values at out (device memory,
+ * 2*n_elems bytes, 2-byte aligned) -- the whole of Algorithm 1 on the GPU.
+ * All stream pointers are device pointers.  One transformer block encoded
+ * as one stream decodes in one launch (Sec. 2.3.3).  The work is enqueued
+ * on `stream` and the call returns without waiting; buffers must stay alive
+ * until the stream has executed it.  n_elems == 0 launches nothing.
+ * Returns DF11_E_UNSUPPORTED for bytes_per_thread != 8, DF11_E_HIP when the
+ * launch fails. */
+int df11_decode_block(const df11_stream *dev, uint16_t *out, hipStream_t stream);
+
+/* Launch shape df11_decode_block would use on the current device for this
+ * stream: workgroups, threads per workgroup and LDS bytes per workgroup. */
+int df11_decode_launch_shape(const df11_stream *dev, uint32_t *grid, uint32_t *block,
+                             uint32_t *lds_bytes);
+
+/* Static description of a status code. */
+const char *df11_strerror(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DF11_H */

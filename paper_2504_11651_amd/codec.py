@@ -1,0 +1,285 @@
+"""Thin ctypes binding of libdf11.so (the C ABI declared in include/df11.h).
+
+Argument marshalling only: every step of encoding runs in the library's C++
+host code and every step of decoding in its HIP kernels.  PyTorch supplies
+device memory and the current HIP stream; nothing here computes.  When the
+library is missing, import fails loudly -- there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libdf11.so")
+
+DF11_OK = 0
+ERRORS = {
+    -1: "DF11_E_INVALID_ARG", -2: "DF11_E_CAP_INFEASIBLE", -3: "DF11_E_BUFFER_TOO_SMALL",
+    -4: "DF11_E_CORRUPT", -5: "DF11_E_HIP", -6: "DF11_E_UNSUPPORTED",
+}
+
+# every function include/df11.h declares
+EXPORTS = (
+    "df11_build_codebook", "df11_codebook_from_counts", "df11_encoded_sizes", "df11_encode",
+    "df11_build_tables", "df11_validate", "df11_decode_block", "df11_decode_launch_shape",
+    "df11_strerror",
+)
+
+
+class Codebook(ctypes.Structure):
+    _fields_ = [("max_code_len", ctypes.c_uint32), ("num_symbols", ctypes.c_uint32),
+                ("count", ctypes.c_uint64 * 256), ("len", ctypes.c_uint8 * 256),
+                ("code", ctypes.c_uint32 * 256)]
+
+    @property
+    def lengths(self) -> np.ndarray:
+        return np.frombuffer(bytes(self.len), np.uint8).copy()
+
+    @property
+    def codes(self) -> np.ndarray:
+        return np.array(self.code[:], np.uint32)
+
+    @property
+    def counts(self) -> np.ndarray:
+        return np.array(self.count[:], np.uint64)
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [("bytes_per_thread", ctypes.c_uint32), ("threads_per_block", ctypes.c_uint32),
+                ("lut_bits", ctypes.c_uint32)]
+
+
+class Sizes(ctypes.Structure):
+    _fields_ = [("n_elems", ctypes.c_uint64), ("total_bits", ctypes.c_uint64),
+                ("num_chunks", ctypes.c_uint64), ("num_blocks", ctypes.c_uint64),
+                ("exp_bytes", ctypes.c_uint64), ("sm_bytes", ctypes.c_uint64),
+                ("gap_bytes", ctypes.c_uint64), ("block_pos_bytes", ctypes.c_uint64),
+                ("table_bytes", ctypes.c_uint64), ("max_elems_per_block", ctypes.c_uint32),
+                ("max_code_len", ctypes.c_uint32)]
+
+    def as_dict(self) -> dict:
+        return {k: int(getattr(self, k)) for k, _ in self._fields_}
+
+
+class Stream(ctypes.Structure):
+    _fields_ = [("exp", ctypes.c_void_p), ("sm", ctypes.c_void_p), ("gaps", ctypes.c_void_p),
+                ("block_pos", ctypes.c_void_p), ("tables", ctypes.c_void_p), ("sizes", Sizes),
+                ("layout", Layout)]
+
+
+DEFAULT_LAYOUT = (8, 256, 12)  # bytes per thread, threads per block, table index bits
+
+_lib = None
+
+
+class DF11Error(RuntimeError):
+    def __init__(self, rc: int, what: str):
+        super().__init__(f"{what}: {ERRORS.get(rc, rc)} ({rc})")
+        self.rc = rc
+
+
+def lib():
+    """The loaded libdf11.so; raises when it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                          "(there is no fallback decoder)")
+    L = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    vp = ctypes.c_void_p
+    u64 = ctypes.c_uint64
+    sig = {
+        "df11_build_codebook": [vp, u64, ctypes.c_uint32, P(Codebook)],
+        "df11_codebook_from_counts": [vp, ctypes.c_uint32, P(Codebook)],
+        "df11_encoded_sizes": [P(Codebook), P(Layout), P(Sizes)],
+        "df11_encode": [vp, u64, P(Codebook), P(Layout), vp, u64, vp, u64, vp, u64, vp, u64,
+                        P(Sizes)],
+        "df11_build_tables": [P(Codebook), ctypes.c_uint32, vp, u64],
+        "df11_validate": [P(Stream)],
+        "df11_decode_block": [P(Stream), vp, vp],
+        "df11_decode_launch_shape": [P(Stream), P(ctypes.c_uint32), P(ctypes.c_uint32),
+                                     P(ctypes.c_uint32)],
+    }
+    for name, args in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    L.df11_strerror.argtypes = [ctypes.c_int]
+    L.df11_strerror.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _check(rc: int, what: str):
+    if rc != DF11_OK:
+        raise DF11Error(rc, what)
+
+
+def _u16(w) -> np.ndarray:
+    a = np.ascontiguousarray(w)
+    if a.dtype != np.uint16:
+        a = a.view(np.uint16)
+    return a.reshape(-1)
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data) if a.size else ctypes.c_void_p(0)
+
+
+def make_layout(bytes_per_thread=None, threads_per_block=None, lut_bits=None) -> Layout:
+    n, T, K = DEFAULT_LAYOUT
+    return Layout(bytes_per_thread or n, threads_per_block or T, lut_bits or K)
+
+
+# ---------------------------------------------------------------- host side
+def build_codebook(w, max_code_len: int = 32) -> Codebook:
+    w = _u16(w)
+    cb = Codebook()
+    _check(lib().df11_build_codebook(_ptr(w), w.size, max_code_len, ctypes.byref(cb)),
+           "df11_build_codebook")
+    return cb
+
+
+def codebook_from_counts(counts, max_code_len: int = 32) -> Codebook:
+    c = np.ascontiguousarray(counts, dtype=np.uint64)
+    cb = Codebook()
+    _check(lib().df11_codebook_from_counts(_ptr(c), max_code_len, ctypes.byref(cb)),
+           "df11_codebook_from_counts")
+    return cb
+
+
+def encoded_sizes(cb: Codebook, layout: Layout) -> Sizes:
+    s = Sizes()
+    _check(lib().df11_encoded_sizes(ctypes.byref(cb), ctypes.byref(layout), ctypes.byref(s)),
+           "df11_encoded_sizes")
+    return s
+
+
+def build_tables(cb: Codebook, lut_bits: int) -> np.ndarray:
+    lay = Layout(8, 256, lut_bits)
+    nbytes = encoded_sizes(cb, lay).table_bytes
+    t = np.zeros(nbytes, np.uint8)
+    _check(lib().df11_build_tables(ctypes.byref(cb), lut_bits, _ptr(t), t.size),
+           "df11_build_tables")
+    return t
+
+
+@dataclass
+class HostStream:
+    """One encoded stream in host memory (numpy arrays)."""
+    exp: np.ndarray
+    sm: np.ndarray
+    gaps: np.ndarray
+    block_pos: np.ndarray
+    tables: np.ndarray
+    sizes: Sizes
+    layout: Layout
+    codebook: Codebook
+
+    def struct(self) -> Stream:
+        return Stream(_ptr(self.exp).value, _ptr(self.sm).value, _ptr(self.gaps).value,
+                      _ptr(self.block_pos).value, _ptr(self.tables).value, self.sizes,
+                      self.layout)
+
+    @property
+    def compressed_bytes(self) -> int:
+        """Bytes the decoder reads: exact stream + sign/mantissa + gaps + positions + tables."""
+        z = self.sizes
+        return int((z.total_bits + 7) // 8 + z.sm_bytes + z.gap_bytes + z.block_pos_bytes +
+                   z.table_bytes)
+
+
+def encode(w, cb: Codebook | None = None, layout: Layout | None = None,
+           max_code_len: int = 32) -> HostStream:
+    """Code book (unless given), stream, metadata and tables for BF16 bit patterns."""
+    w = _u16(w)
+    layout = layout or make_layout()
+    if cb is None:
+        cb = build_codebook(w, max_code_len)
+    z = encoded_sizes(cb, layout)
+    exp = np.empty(z.exp_bytes, np.uint8)
+    sm = np.empty(max(z.sm_bytes, 1), np.uint8)
+    gaps = np.empty(z.gap_bytes, np.uint8)
+    bp = np.empty(z.num_blocks + 1, np.uint32)
+    out = Sizes()
+    _check(lib().df11_encode(_ptr(w), w.size, ctypes.byref(cb), ctypes.byref(layout), _ptr(exp),
+                             exp.size, _ptr(sm), sm.size, _ptr(gaps), gaps.size, _ptr(bp),
+                             bp.nbytes, ctypes.byref(out)), "df11_encode")
+    tables = build_tables(cb, layout.lut_bits)
+    return HostStream(exp, sm[:z.sm_bytes], gaps, bp, tables, out, layout, cb)
+
+
+def validate(hs: HostStream) -> int:
+    """0 when consistent, else the negative status (no exception)."""
+    st = hs.struct()
+    return int(lib().df11_validate(ctypes.byref(st)))
+
+
+def strerror(rc: int) -> str:
+    return lib().df11_strerror(rc).decode()
+
+
+# ---------------------------------------------------------------- device side
+class DeviceStream:
+    """A stream resident in device memory (torch uint8/int32 tensors)."""
+
+    def __init__(self, hs: HostStream, device="cuda"):
+        import torch
+        dev = torch.device(device)
+        self.exp = torch.from_numpy(hs.exp).to(dev)
+        self.sm = torch.from_numpy(hs.sm if hs.sm.size else np.zeros(1, np.uint8)).to(dev)
+        self.gaps = torch.from_numpy(hs.gaps).to(dev)
+        self.block_pos = torch.from_numpy(hs.block_pos.view(np.int32)).to(dev)
+        self.tables = torch.from_numpy(hs.tables).to(dev)
+        self.sizes = Sizes.from_buffer_copy(hs.sizes)
+        self.layout = Layout.from_buffer_copy(hs.layout)
+        self.device = dev
+        self._st = Stream(self.exp.data_ptr(), self.sm.data_ptr(), self.gaps.data_ptr(),
+                          self.block_pos.data_ptr(), self.tables.data_ptr(), self.sizes,
+                          self.layout)
+
+    @property
+    def n_elems(self) -> int:
+        return int(self.sizes.n_elems)
+
+    def struct(self) -> Stream:
+        return self._st
+
+    def nbytes(self) -> int:
+        return sum(t.numel() * t.element_size()
+                   for t in (self.exp, self.sm, self.gaps, self.block_pos, self.tables))
+
+
+def to_device(hs: HostStream, device="cuda") -> DeviceStream:
+    return DeviceStream(hs, device)
+
+
+def launch_shape(ds: DeviceStream):
+    g, b, l = ctypes.c_uint32(), ctypes.c_uint32(), ctypes.c_uint32()
+    _check(lib().df11_decode_launch_shape(ctypes.byref(ds.struct()), ctypes.byref(g),
+                                          ctypes.byref(b), ctypes.byref(l)),
+           "df11_decode_launch_shape")
+    return int(g.value), int(b.value), int(l.value)
+
+
+def decode_block(ds: DeviceStream, out=None, stream=None):
+    """Decode into ``out`` (a bfloat16 device tensor of n_elems, 16-byte aligned;
+    allocated when None) on ``stream`` (default: torch's current stream)."""
+    import torch
+    n = ds.n_elems
+    if out is None:
+        out = torch.empty(n, dtype=torch.bfloat16, device=ds.device)
+    if out.numel() < n or out.element_size() != 2 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous 2-byte tensor with n_elems elements")
+    if stream is None:
+        stream = torch.cuda.current_stream(ds.device)
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    _check(lib().df11_decode_block(ctypes.byref(ds.struct()), ctypes.c_void_p(out.data_ptr()),
+                                   ctypes.c_void_p(handle)), "df11_decode_block")
+    return out

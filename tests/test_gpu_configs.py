@@ -1,0 +1,101 @@
+"""GPU parity at full workload sizes, in the launch configuration the
+benchmark times (default layout: n = 8 bytes per thread, T = 256, 12-bit
+table).  Every decoded weight is compared with the generator's input (a
+property that holds at any size, given the oracle's pinned round trip); the
+library's stream is compared byte for byte with the oracle's own stream, and
+sampled blocks are decoded by the oracle and compared with the GPU output."""
+import functools
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_11651_amd import codec, synth
+
+from conftest import gpu_available
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs an MI355X")]
+
+
+@functools.lru_cache(maxsize=1)
+def weights(name: str) -> np.ndarray:
+    if name == "matrix_4096":
+        return synth.matrix_4096()
+    if name == "llama3_8b_block":
+        return synth.llama3_8b_block()[0]
+    if name == "heavy_tailed_block":
+        return synth.heavy_tailed_block()
+    if name == "llama31_70b_block":
+        return synth.llama31_70b_block()[0]
+    if name == "fibonacci_40":
+        return synth.fibonacci_exponents(40)
+    raise KeyError(name)
+
+
+def decode_on_gpu(hs):
+    import torch
+    ds = codec.to_device(hs, "cuda")
+    out = torch.full((ds.n_elems,), 0x5A5A, dtype=torch.int16, device="cuda")
+    codec.decode_block(ds, out.view(torch.bfloat16))
+    torch.cuda.synchronize()
+    del ds
+    return out
+
+
+def check_full(w: np.ndarray, out) -> None:
+    import torch
+    ref = torch.from_numpy(w.view(np.int16)).to(out.device)
+    same = out == ref
+    if not bool(same.all()):
+        bad = torch.nonzero(~same).flatten()[:8].cpu().tolist()
+        pytest.fail(f"{int((~same).sum())} mismatches, first at {bad}")
+
+
+def check_against_oracle_stream(w, hs, out, sample_blocks=12, seed=0):
+    """Oracle's own stream == library stream; oracle block decode == GPU."""
+    st = oracle.compress(w, 32, 8, hs.layout.threads_per_block)
+    assert np.array_equal(st["lengths"], hs.codebook.lengths)
+    assert st["total_bits"] == hs.sizes.total_bits
+    assert np.array_equal(st["exp"], hs.exp)
+    assert np.array_equal(st["sm"], hs.sm)
+    assert np.array_equal(st["gaps_packed"], hs.gaps)
+    assert np.array_equal(st["block_pos"], hs.block_pos)
+    B = st["num_blocks"]
+    rng = np.random.default_rng(seed)
+    blocks = sorted(set([0, B - 1] + rng.integers(0, B, size=sample_blocks).tolist()))
+    got = out.view(-1)
+    ref = np.zeros(w.size, np.uint16)
+    for b in blocks:
+        oracle.decode_blocks(st["exp"], st["total_bits"], st["sm"], w.size, st["lengths"], 8,
+                             hs.layout.threads_per_block, st["gaps"], st["block_pos"], b, 1, ref)
+        lo, hi = int(st["block_pos"][b]), int(st["block_pos"][b + 1])
+        g = got[lo:hi].cpu().numpy().view(np.uint16)
+        assert np.array_equal(g, ref[lo:hi]), f"block {b}"
+
+
+@pytest.mark.parametrize("name", ["matrix_4096", "llama3_8b_block", "heavy_tailed_block"])
+def test_config_bit_exact_and_oracle_stream(name):
+    w = weights(name)
+    hs = codec.encode(w)
+    assert codec.validate(hs) == 0
+    out = decode_on_gpu(hs)
+    check_full(w, out)
+    check_against_oracle_stream(w, hs, out)
+
+
+def test_llama31_70b_block_bit_exact():
+    w = weights("llama31_70b_block")
+    assert w.size == 855_638_016
+    hs = codec.encode(w)
+    out = decode_on_gpu(hs)
+    check_full(w, out)
+    check_against_oracle_stream(w, hs, out, sample_blocks=8, seed=4)
+
+
+def test_fibonacci_cap_binds_32_bit_codes():
+    w = weights("fibonacci_40")
+    hs = codec.encode(w)
+    assert hs.codebook.max_code_len == 32
+    out = decode_on_gpu(hs)
+    check_full(w, out)

@@ -1,0 +1,121 @@
+"""GPU parity: the HIP decoder (through the C ABI) against the oracle, element
+by element, on small and edge-case streams under several launch layouts."""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_11651_amd import codec, synth
+
+from conftest import gpu_available
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not gpu_available(), reason="needs an MI355X")]
+
+CASES = {
+    "one": lambda: np.array([0xBF80], np.uint16),
+    "two": lambda: np.array([0x3F80, 0x0001], np.uint16),
+    "seventeen": lambda: synth.gaussian(17, 0.02, 17),
+    "single_symbol": lambda: (np.arange(70_001, dtype=np.uint16) & 0x807F) | (100 << 7),
+    "gauss_1000": lambda: synth.gaussian(1000, 0.02, 1),
+    "gauss_65537": lambda: synth.gaussian(65_537, 0.02, 2),
+    "gauss_1m": lambda: synth.gaussian(1_000_003, 0.02, 3),
+    "gauss_wide": lambda: synth.gaussian(300_000, 5.0, 4),
+    "special": lambda: synth.special_values(200_000),
+    "patterns": synth.all_bf16_patterns,
+    "fib24": lambda: synth.fibonacci_exponents(24),
+    "heavy": lambda: synth.heavy_tailed_block(500_000, 2),
+}
+LAYOUTS = [(8, 64, 8), (8, 128, 10), (8, 256, 12), (8, 512, 11), (8, 1024, 12)]
+
+
+def oracle_reference(w: np.ndarray, cap: int = 32) -> np.ndarray:
+    st = oracle.compress(w, cap, 8, 256)
+    ref = oracle.decode_serial(st["exp"], st["total_bits"], st["sm"], w.size, st["lengths"])
+    assert np.array_equal(ref, w)
+    return ref
+
+
+def gpu_decode(hs, poison: int, guard: int = 64, stream=None):
+    import torch
+    ds = codec.to_device(hs, "cuda")
+    n = ds.n_elems
+    buf = torch.full((n + guard,), poison, dtype=torch.int16, device="cuda")
+    codec.decode_block(ds, buf[:n].view(torch.bfloat16), stream=stream)
+    torch.cuda.synchronize()
+    host = buf.cpu().numpy().view(np.uint16)
+    assert (host[n:] == np.uint16(poison & 0xFFFF)).all(), "decoder wrote past the output"
+    return host[:n]
+
+
+@pytest.mark.parametrize("lay", LAYOUTS, ids=lambda l: "T%d_K%d" % l[1:])
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_decode_matches_oracle(case, lay):
+    w = CASES[case]()
+    ref = oracle_reference(w)
+    hs = codec.encode(w, layout=codec.make_layout(*lay))
+    for poison in (0x5555, -0x5556):  # two patterns: every element must be written
+        got = gpu_decode(hs, poison)
+        bad = np.flatnonzero(got != ref)
+        assert bad.size == 0, f"{bad.size} mismatches, first {bad[:8].tolist()}"
+
+
+@pytest.mark.parametrize("cap,K", [(12, 8), (10, 8), (16, 9)])
+def test_long_codes_through_escape_path(cap, K):
+    """Capped Fibonacci histogram: most code lengths exceed the table width."""
+    w = synth.fibonacci_exponents(28)
+    ref = oracle_reference(w, cap)
+    hs = codec.encode(w, layout=codec.make_layout(8, 256, K), max_code_len=cap)
+    assert hs.codebook.max_code_len == cap
+    got = gpu_decode(hs, 0x1234)
+    assert np.array_equal(got, ref)
+
+
+def test_empty_stream_launches_nothing():
+    import torch
+    hs = codec.encode(np.zeros(0, np.uint16))
+    ds = codec.to_device(hs, "cuda")
+    out = torch.full((8,), 7, dtype=torch.int16, device="cuda")
+    codec.decode_block(ds, out.view(torch.bfloat16))
+    torch.cuda.synchronize()
+    assert (out.cpu() == 7).all()
+
+
+def test_decode_is_deterministic_and_stream_ordered():
+    import torch
+    w = synth.gaussian(2_000_000, 0.03, 9)
+    hs = codec.encode(w)
+    ds = codec.to_device(hs, "cuda")
+    s = torch.cuda.Stream()
+    outs = []
+    for _ in range(3):
+        o = torch.empty(w.size, dtype=torch.bfloat16, device="cuda")
+        with torch.cuda.stream(s):
+            codec.decode_block(ds, o, stream=s)
+        outs.append(o)
+    s.synchronize()
+    for o in outs:
+        assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16))
+    assert np.array_equal(outs[0].view(torch.int16).cpu().numpy().view(np.uint16), w)
+
+
+def test_decode_into_aligned_view_of_workspace():
+    import torch
+    w = synth.gaussian(123_457, 0.02, 10)
+    hs = codec.encode(w)
+    ds = codec.to_device(hs, "cuda")
+    ws = torch.full((w.size + 1024,), -1, dtype=torch.int16, device="cuda")
+    view = ws[512:512 + w.size]  # 1 KiB offset keeps 16-byte alignment
+    codec.decode_block(ds, view.view(torch.bfloat16))
+    torch.cuda.synchronize()
+    host = ws.cpu().numpy().view(np.uint16)
+    assert np.array_equal(host[512:512 + w.size], w)
+    assert (host[:512] == 0xFFFF).all() and (host[512 + w.size:] == 0xFFFF).all()
+
+
+def test_misaligned_output_is_rejected():
+    import torch
+    hs = codec.encode(synth.gaussian(1000, 0.02, 1))
+    ds = codec.to_device(hs, "cuda")
+    ws = torch.empty(2000, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(codec.DF11Error):
+        codec.decode_block(ds, ws[1:1001])
