@@ -157,7 +157,7 @@ def main() -> int:
 
     z = hs.sizes
     exp_bytes_exact = (int(z.total_bits) + 7) // 8
-    read_bytes = exp_bytes_exact + int(z.sm_bytes) + int(z.gap_bytes) + int(z.block_pos_bytes) + \
+    read_bytes = exp_bytes_exact + n + int(z.gap_bytes) + int(z.block_pos_bytes) + \
         int(z.table_bytes)
     write_bytes = 2 * n
     algo_bytes = read_bytes + write_bytes

@@ -27,6 +27,9 @@
  *     gap_bytes = 4*(ceil(5*(B*T+1)/32)+2) bytes;
  *   - BlockOutputPos[b] = number of codes starting before bit 8n*T*b, for
  *     b = 0 .. B (B+1 entries; the last is n_elems);
+ *   - PackedSignMantissa holds n_elems bytes followed by zero padding up to
+ *     sm_bytes = (n_elems rounded up to 16) + 16, so whole 8-byte groups can
+ *     always be read;
  *   - all 256 exponent values are codable (the paper's format reserves
  *     240..255 as table pointers; this one does not need to);
  *   - code lengths are capped at max_code_len <= 32 (gaps fit 5 bits); when
@@ -83,7 +86,8 @@ typedef struct {
     uint64_t num_chunks;          /* C */
     uint64_t num_blocks;          /* B */
     uint64_t exp_bytes;           /* EncodedExponent bytes incl. padding */
-    uint64_t sm_bytes;            /* PackedSignMantissa bytes (= n_elems) */
+    uint64_t sm_bytes;            /* PackedSignMantissa buffer: n_elems bytes, zero padded to
+                                     a multiple of 16, plus 16 */
     uint64_t gap_bytes;           /* packed Gaps bytes */
     uint64_t block_pos_bytes;     /* 4 * (B + 1) */
     uint64_t table_bytes;         /* decode-table blob bytes */

@@ -71,7 +71,7 @@ class Stream(ctypes.Structure):
                 ("layout", Layout)]
 
 
-DEFAULT_LAYOUT = (8, 256, 12)  # bytes per thread, threads per block, table index bits
+DEFAULT_LAYOUT = (8, 64, 12)  # bytes per thread, threads per block, table index bits
 
 _lib = None
 
@@ -174,7 +174,7 @@ def build_tables(cb: Codebook, lut_bits: int) -> np.ndarray:
 class HostStream:
     """One encoded stream in host memory (numpy arrays)."""
     exp: np.ndarray
-    sm: np.ndarray
+    sm: np.ndarray  # n_elems bytes + zero padding (sizes.sm_bytes)
     gaps: np.ndarray
     block_pos: np.ndarray
     tables: np.ndarray
@@ -191,7 +191,7 @@ class HostStream:
     def compressed_bytes(self) -> int:
         """Bytes the decoder reads: exact stream + sign/mantissa + gaps + positions + tables."""
         z = self.sizes
-        return int((z.total_bits + 7) // 8 + z.sm_bytes + z.gap_bytes + z.block_pos_bytes +
+        return int((z.total_bits + 7) // 8 + z.n_elems + z.gap_bytes + z.block_pos_bytes +
                    z.table_bytes)
 
 
@@ -204,7 +204,7 @@ def encode(w, cb: Codebook | None = None, layout: Layout | None = None,
         cb = build_codebook(w, max_code_len)
     z = encoded_sizes(cb, layout)
     exp = np.empty(z.exp_bytes, np.uint8)
-    sm = np.empty(max(z.sm_bytes, 1), np.uint8)
+    sm = np.empty(z.sm_bytes, np.uint8)
     gaps = np.empty(z.gap_bytes, np.uint8)
     bp = np.empty(z.num_blocks + 1, np.uint32)
     out = Sizes()
@@ -212,7 +212,7 @@ def encode(w, cb: Codebook | None = None, layout: Layout | None = None,
                              exp.size, _ptr(sm), sm.size, _ptr(gaps), gaps.size, _ptr(bp),
                              bp.nbytes, ctypes.byref(out)), "df11_encode")
     tables = build_tables(cb, layout.lut_bits)
-    return HostStream(exp, sm[:z.sm_bytes], gaps, bp, tables, out, layout, cb)
+    return HostStream(exp, sm, gaps, bp, tables, out, layout, cb)
 
 
 def validate(hs: HostStream) -> int:
@@ -233,7 +233,7 @@ class DeviceStream:
         import torch
         dev = torch.device(device)
         self.exp = torch.from_numpy(hs.exp).to(dev)
-        self.sm = torch.from_numpy(hs.sm if hs.sm.size else np.zeros(1, np.uint8)).to(dev)
+        self.sm = torch.from_numpy(hs.sm).to(dev)
         self.gaps = torch.from_numpy(hs.gaps).to(dev)
         self.block_pos = torch.from_numpy(hs.block_pos.view(np.int32)).to(dev)
         self.tables = torch.from_numpy(hs.tables).to(dev)

@@ -1,26 +1,31 @@
 // DFloat11 decompression on gfx950 (Algorithm 1 of arXiv 2504.11651,
 // re-designed for CDNA4).
 //
-// One workgroup decodes one block of T chunks at a time (the paper's
-// "thread block"); a persistent grid walks the blocks so the decode tables
-// are staged into LDS once per workgroup instead of once per block.
+// A block of T chunks (the paper's "thread block") is decoded by one
+// wavefront when T = 64 -- the block's prefix sum is then a wave-level DPP
+// scan and no workgroup barrier is needed, so the waves of a CU drift into
+// different phases and decode overlaps memory streaming -- or by one
+// workgroup when T >= 128.  The grid is persistent: decode tables are staged
+// into LDS once per workgroup and shared by all of its waves.
 //
 // Per block:
 //   1. every lane loads its 8-byte chunk of EncodedExponent plus the next
 //      4 bytes, and its two 5-bit Gaps (own chunk and next chunk);
 //   2. phase 1 (count): starting at the gap, decode with the multi-symbol
 //      table until the code start reaches the next chunk's first code;
-//   3. workgroup exclusive scan of the counts (wave scan + LDS across waves)
-//      gives each lane its output position (Sec. 2.3.2);
+//   3. exclusive scan of the counts (wave DPP scan, plus LDS across waves
+//      for T >= 128) gives each lane its output position (Sec. 2.3.2);
 //   4. phase 2 (emit): decode again and OR the exponent bytes into an LDS
 //      buffer at their output positions.  A lookup may run past the lane's
 //      last code; the extra codes are the next lanes' first codes, decoded
 //      from the same bits, so they land on their own positions with their
 //      own values and need no masking;
 //   5. assemble BF16 = sign<<15 | exponent<<7 | mantissa (Algorithm 1) for
-//      16 consecutive outputs per lane: one 16-byte PackedSignMantissa load,
-//      one 16-byte LDS read, two 16-byte stores -- coalesced, no per-element
-//      gather (the paper gathers sign/mantissa per element).
+//      8 consecutive outputs per lane and step: one 8-byte PackedSignMantissa
+//      load (issued when the block starts), one 8-byte LDS read, one 16-byte
+//      store; consecutive lanes take consecutive groups, so a wave stores
+//      1 KiB contiguous per instruction.  No per-element gather (the paper
+//      gathers sign/mantissa per element).
 // Integer work only; no MFMA.
 #include <hip/hip_runtime.h>
 
@@ -34,7 +39,7 @@
 namespace {
 
 constexpr uint32_t kScanSlots = 16;  // waves per workgroup (<= 1024 threads)
-constexpr uint32_t kBufSlack = 32;   // alignment shift (< 16) + over-decoded bytes
+constexpr uint32_t kBufSlack = 32;   // alignment shift (< 8) + over-decoded bytes
 
 struct DecodeArgs {
     const uint8_t *exp;
@@ -59,7 +64,7 @@ __device__ __forceinline__ uint32_t lsb_first(uint32_t le) {
     return __builtin_bitreverse32(__builtin_bswap32(le));
 }
 
-// 32 stream bits starting at bit p (0 <= p < 64) of the 96 bits w0:w1:w2.
+// 32 bits starting at bit p (0 <= p < 64) of the 96 bits w0:w1:w2.
 __device__ __forceinline__ uint32_t window_at(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t p) {
     const bool upper = p >= 32;
     const uint32_t lo = upper ? w1 : w0;
@@ -68,18 +73,31 @@ __device__ __forceinline__ uint32_t window_at(uint32_t w0, uint32_t w1, uint32_t
 }
 
 struct Tables {
-    const uint2 *ent;        // K-bit entries: x = exponents, y = meta
+    const uint8_t *ent;      // K-bit entries, 8 bytes: x = exponents, y = meta
     const uint32_t *lj_last; // [33]
     const uint32_t *offset;  // [33]
     const uint8_t *sorted;   // [256]
-    uint32_t mask;
+    uint32_t addr_mask;      // (2^K - 1) << 3: entry byte offset from a shifted window
     uint32_t lut_bits;
     uint32_t max_len;
 };
 
+__device__ __forceinline__ Tables stage_tables(const DecodeArgs &a, uint8_t *lds) {
+    Tables tb;
+    const uint32_t ent_bytes = 8u << a.lut_bits;
+    tb.ent = lds;
+    tb.lj_last = reinterpret_cast<const uint32_t *>(lds + ent_bytes);
+    tb.offset = tb.lj_last + 33;
+    tb.sorted = reinterpret_cast<const uint8_t *>(tb.offset + 33);
+    tb.addr_mask = ((1u << a.lut_bits) - 1u) << 3;
+    tb.lut_bits = a.lut_bits;
+    tb.max_len = a.max_len;
+    return tb;
+}
+
 // Code longer than the table index: canonical length search on the
 // left-justified window, then rank within the length.
-__device__ __forceinline__ uint2 decode_long(Tables t, uint32_t win) {
+__device__ __forceinline__ uint2 decode_long(const Tables &t, uint32_t win) {
     const uint32_t v = __builtin_bitreverse32(win);
     uint32_t L = t.lut_bits + 1;
     while (L < t.max_len && v > t.lj_last[L]) ++L;
@@ -87,20 +105,25 @@ __device__ __forceinline__ uint2 decode_long(Tables t, uint32_t win) {
     return make_uint2(t.sorted[idx], L | (1u << 8) | (1u << 16));
 }
 
-__device__ __forceinline__ uint2 lookup(Tables t, uint32_t win) {
-    uint2 e = t.ent[win & t.mask];
-    if (e.y == 0) e = decode_long(t, win);
-    return e;
+// Inclusive prefix sum over the 64 lanes of a wave: four row shifts give the
+// sums within each row of 16 lanes, two row broadcasts carry row totals.
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t v) {
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xF, 0xF, true));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xF, 0xF, true));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x114, 0xF, 0xF, true));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, true));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x142, 0xA, 0xF, false));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x143, 0xC, 0xF, false));
+    return v;
 }
 
-__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t v) {
-    const uint32_t lane = __lane_id();
-#pragma unroll
-    for (uint32_t d = 1; d < 64; d <<= 1) {
-        const uint32_t t = __shfl_up(v, d, 64);
-        if (lane >= d) v += t;
-    }
-    return v;
+// Orders this wave's LDS accesses (other lanes' writes become visible to
+// later reads: LDS executes a wave's instructions in order; this keeps the
+// compiler from moving accesses across).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
 // 4 sign/mantissa bytes + 4 exponents -> 4 BF16 (two words, low element first).
@@ -111,135 +134,346 @@ __device__ __forceinline__ void assemble4(uint32_t S, uint32_t E, uint32_t &o0, 
     o1 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
 }
 
-template <uint32_t T>
-__global__ __launch_bounds__(T) void df11_decode_kernel(DecodeArgs a) {
+// Raw global words one lane needs for chunk c of block b: the chunk's 8
+// bytes, the next 4 bytes, the two 32-bit words holding Gaps[c] and
+// Gaps[c+1], and the block's two BlockOutputPos entries.
+struct ChunkWords {
+    uint32_t x, y, z, g0, g1, bp0, bp1;
+};
+
+__device__ __forceinline__ ChunkWords load_chunk(const DecodeArgs &a, uint32_t b, uint32_t c) {
+    ChunkWords r;
+    r.bp0 = a.block_pos[b];
+    r.bp1 = a.block_pos[b + 1];
+    const uint2 own = *reinterpret_cast<const uint2 *>(a.exp + 8ull * c);
+    r.x = own.x;
+    r.y = own.y;
+    r.z = *reinterpret_cast<const uint32_t *>(a.exp + 8ull * c + 8);
+    const uint64_t gw = (5ull * c) >> 5;
+    r.g0 = a.gaps[gw];
+    r.g1 = a.gaps[gw + 1];
+    return r;
+}
+
+// Lookups kept in registers between the count phase and the write phase;
+// a chunk needing more (short codes, 4 per lookup) continues in a loop.
+constexpr int kKeep = 12;
+// 8-element output groups whose sign/mantissa bytes are fetched at block start.
+constexpr int kPre = 4;
+
+// One chunk's decode state.  w*: the chunk's bits (word j bit i = stream bit
+// 32j+i); s*: the same bits moved up by 3, so that a window taken from s* at
+// bit p holds stream bits p.. at bits 3.. and masking it gives the byte
+// offset of the table entry directly.
+struct Chunk {
+    uint32_t w0, w1, w2, s0, s1, s2, start, end;
+};
+
+__device__ __forceinline__ Chunk chunk_setup(const DecodeArgs &a, const ChunkWords &cw, uint32_t c) {
+    Chunk ch;
+    ch.w0 = lsb_first(cw.x);
+    ch.w1 = lsb_first(cw.y);
+    ch.w2 = lsb_first(cw.z);
+    ch.s0 = ch.w0 << 3;
+    ch.s1 = __builtin_amdgcn_alignbit(ch.w1, ch.w0, 29);
+    ch.s2 = __builtin_amdgcn_alignbit(ch.w2, ch.w1, 29);
+    const uint64_t gv = ((static_cast<uint64_t>(__builtin_bswap32(cw.g0)) << 32) |
+                         __builtin_bswap32(cw.g1))
+                        << ((5u * c) & 31u);
+    const uint32_t gap_own = static_cast<uint32_t>(gv >> 59);
+    const uint32_t gap_next = static_cast<uint32_t>(gv >> 54) & 31u;
+    ch.start = 0;
+    ch.end = 0;
+    if (c < a.num_chunks) {
+        ch.start = gap_own;
+        const uint32_t e = (c + 1 < a.num_chunks) ? 64u + gap_next
+                                                  : static_cast<uint32_t>(a.total_bits - 64ull * c);
+        ch.end = min(e, 95u);
+    }
+    return ch;
+}
+
+__device__ __forceinline__ uint2 lookup(const Tables &t, const Chunk &ch, uint32_t p) {
+    const uint32_t ws = window_at(ch.s0, ch.s1, ch.s2, p);
+    uint2 e = *reinterpret_cast<const uint2 *>(t.ent + (ws & t.addr_mask));
+    if (e.y == 0u) e = decode_long(t, window_at(ch.w0, ch.w1, ch.w2, p));
+    return e;
+}
+
+// Phase 1: decode the codes that start in the chunk, keep up to kKeep
+// lookups (exponent words in sy, code counts one byte each in npk), and
+// count the codes.  Returns the count; *p_rest = where decoding stopped.
+__device__ __forceinline__ uint32_t decode_count(const Tables &t, const Chunk &ch,
+                                                 uint32_t (&sy)[kKeep],
+                                                 uint32_t (&npk)[(kKeep + 3) / 4],
+                                                 uint32_t *p_rest) {
+#pragma unroll
+    for (int k = 0; k < (kKeep + 3) / 4; ++k) npk[k] = 0u;
+    uint32_t p = ch.start, cnt = 0, last_p = 0, last_meta = 0;
+#pragma unroll
+    for (int k = 0; k < kKeep; ++k) {
+        const bool act = p < ch.end;
+        sy[k] = 0u;
+        if (__builtin_amdgcn_ballot_w64(act) == 0) continue;  // wave-uniform skip
+        const uint32_t ws = window_at(ch.s0, ch.s1, ch.s2, p);
+        uint2 e = *reinterpret_cast<const uint2 *>(t.ent + (ws & t.addr_mask));
+        if (act && e.y == 0u) e = decode_long(t, window_at(ch.w0, ch.w1, ch.w2, p));
+        const uint32_t m = act ? e.y : 0u;
+        sy[k] = e.x;
+        constexpr uint32_t sel[4] = {0x03020105u, 0x03020500u, 0x03050100u, 0x05020100u};
+        npk[k / 4] = __builtin_amdgcn_perm(m, npk[k / 4], sel[k % 4]);  // byte k%4 <- count
+        last_p = act ? p : last_p;
+        last_meta = act ? m : last_meta;
+        p += e.y & 0xFFu;  // done lanes only move further past `end`
+        cnt += (m >> 8) & 0xFFu;
+    }
+    *p_rest = p;
+    for (uint32_t it = 0; p < ch.end && it < 96u; ++it) {
+        const uint2 e = lookup(t, ch, p);
+        last_p = p;
+        last_meta = e.y;
+        p += e.y & 0xFFu;
+        cnt += (e.y >> 8) & 0xFFu;
+    }
+    // codes of the last lookup that start at or past `end` belong to the next chunk
+    return cnt - __builtin_popcount((last_meta >> 16) >> min(ch.end - last_p, 31u));
+}
+
+// OR 4 exponent bytes into the zeroed buffer at byte offset off.
+__device__ __forceinline__ void or_exponents(uint32_t *buf32, uint32_t cap_bytes, uint32_t off,
+                                             uint32_t syms) {
+    const uint64_t v = static_cast<uint64_t>(syms) << ((off & 3u) << 3);
+    const uint32_t dw = min(off, cap_bytes) >> 2;
+    atomicOr(&buf32[dw], static_cast<uint32_t>(v));
+    atomicOr(&buf32[dw + 1], static_cast<uint32_t>(v >> 32));
+}
+
+// Phase 2: exponents into the LDS buffer at output offset off (the kept
+// lookups, then the rest of a long chunk by decoding again).
+__device__ __forceinline__ void emit_exponents(const Tables &t, const Chunk &ch,
+                                               const uint32_t (&sy)[kKeep],
+                                               const uint32_t (&npk)[(kKeep + 3) / 4],
+                                               uint32_t p_rest, uint32_t off, uint32_t *buf32,
+                                               uint32_t cap_bytes) {
+#pragma unroll
+    for (int k = 0; k < kKeep; ++k) {
+        const uint32_t n = (npk[k / 4] >> (8 * (k % 4))) & 0xFFu;
+        if (__builtin_amdgcn_ballot_w64(n != 0u) == 0) continue;
+        if (n != 0u) {
+            or_exponents(buf32, cap_bytes, off, sy[k]);
+            off += n;
+        }
+    }
+    uint32_t p = p_rest;
+    for (uint32_t it = 0; p < ch.end && it < 96u; ++it) {
+        const uint2 e = lookup(t, ch, p);
+        or_exponents(buf32, cap_bytes, off, e.x);
+        off += (e.y >> 8) & 0xFFu;
+        p += e.y & 0xFFu;
+    }
+}
+
+// A block's output range, clamped to the buffer and the tensor.
+struct Range {
+    uint32_t s, shift, lim, g0, ngroups;
+};
+
+__device__ __forceinline__ Range block_range(const DecodeArgs &a, const ChunkWords &cw) {
+    Range r;
+    r.s = min(__builtin_amdgcn_readfirstlane(cw.bp0), a.n_elems);
+    uint32_t e = max(min(__builtin_amdgcn_readfirstlane(cw.bp1), a.n_elems), r.s);
+    e = min(e, r.s + (a.buf_bytes - kBufSlack));
+    r.shift = r.s & 7u;
+    r.lim = r.shift + (e - r.s);
+    r.g0 = r.s - r.shift;
+    r.ngroups = (r.lim + 7u) >> 3;
+    return r;
+}
+
+__device__ __forceinline__ bool full_group(const Range &r, uint32_t g) {
+    return (g << 3) >= r.shift && (g << 3) + 8u <= r.lim;
+}
+
+// Sign/mantissa bytes of groups first, first+step, ... (kPre of them).  The
+// buffer is zero padded past n_elems to a multiple of 16 bytes, so a whole
+// group can be read even where the block starts or ends inside it.
+__device__ __forceinline__ void prefetch_sm(const DecodeArgs &a, const Range &r, uint32_t first,
+                                            uint32_t step, uint2 (&S)[kPre]) {
+    const uint32_t last = max(r.ngroups, 1u) - 1u;  // groups past the block reread its last one
+#pragma unroll
+    for (int k = 0; k < kPre; ++k) {
+        const uint32_t g = min(first + k * step, last);
+        S[k] = *reinterpret_cast<const uint2 *>(a.sm + r.g0 + (g << 3));
+    }
+}
+
+// 8 outputs of group g from its sign/mantissa bytes and the exponent buffer.
+__device__ __forceinline__ uint4 assemble_group(const uint8_t *buf, uint32_t g, uint2 Sg) {
+    const uint2 E = reinterpret_cast<const uint2 *>(buf)[g];
+    uint4 o;
+    assemble4(Sg.x, E.x, o.x, o.y);
+    assemble4(Sg.y, E.y, o.z, o.w);
+    return o;
+}
+
+// One 16-byte store, or single-element stores for the elements of a group
+// that the block shares with its neighbour.
+__device__ __forceinline__ void store_group(const DecodeArgs &a, const Range &r, uint32_t g,
+                                            const uint4 &o) {
+    uint16_t *dst = a.out + r.g0 + (g << 3);
+    if (full_group(r, g)) {
+        *reinterpret_cast<uint4 *>(dst) = o;
+        return;
+    }
+    const uint32_t v[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+    for (uint32_t k = 0; k < 8u; ++k) {
+        const uint32_t j = (g << 3) + k;
+        if (j >= r.shift && j < r.lim) dst[k] = static_cast<uint16_t>(v[k >> 1] >> ((k & 1u) * 16u));
+    }
+}
+
+// Outputs of the prefetched groups first + k*step (k < kPre).  Loads and
+// stores share one counter on this GPU, and a wait for a load issued before a
+// pending store has to wait for the store as well; so every prefetched value
+// is consumed here, before any store of the block is issued.
+__device__ __forceinline__ void assemble_prefetched(const Range &r, const uint8_t *buf,
+                                                    uint32_t first, uint32_t step,
+                                                    const uint2 (&S)[kPre], uint4 (&O)[kPre]) {
+#pragma unroll
+    for (int k = 0; k < kPre; ++k) {
+        const uint32_t g = first + k * step;
+        O[k] = make_uint4(0u, 0u, 0u, 0u);
+        if (g < r.ngroups) O[k] = assemble_group(buf, g, S[k]);
+    }
+}
+
+// Stores of the prefetched groups, then the groups past them (a block with
+// more than kPre groups per lane reads their bytes here).
+__device__ __forceinline__ void store_block(const DecodeArgs &a, const Range &r, const uint8_t *buf,
+                                            uint32_t first, uint32_t step, const uint4 (&O)[kPre]) {
+#pragma unroll
+    for (int k = 0; k < kPre; ++k) {
+        const uint32_t g = first + k * step;
+        if (g < r.ngroups) store_group(a, r, g, O[k]);
+    }
+    for (uint32_t g = first + kPre * step; g < r.ngroups; g += step)
+        store_group(a, r, g,
+                    assemble_group(buf, g, *reinterpret_cast<const uint2 *>(a.sm + r.g0 + (g << 3))));
+}
+
+__device__ __forceinline__ void stage_table_blob(const DecodeArgs &a, uint8_t *lds, uint32_t tid,
+                                                 uint32_t nthreads) {
+    const uint4 *src = reinterpret_cast<const uint4 *>(a.tables);
+    uint4 *dst = reinterpret_cast<uint4 *>(lds);
+    for (uint32_t i = tid; i < (a.table_lds_bytes >> 4); i += nthreads) dst[i] = src[i];
+}
+
+// T = 64: every wave owns whole blocks; W waves per workgroup share the tables.
+template <uint32_t W>
+__global__ __launch_bounds__(64 * W) void df11_decode_wave_kernel(DecodeArgs a) {
     extern __shared__ __align__(16) uint8_t lds[];
     const uint32_t tid = threadIdx.x;
-    const uint32_t ent_bytes = 8u << a.lut_bits;
-    Tables tb;
-    tb.ent = reinterpret_cast<const uint2 *>(lds);
-    tb.lj_last = reinterpret_cast<const uint32_t *>(lds + ent_bytes);
-    tb.offset = tb.lj_last + 33;
-    tb.sorted = reinterpret_cast<const uint8_t *>(tb.offset + 33);
-    tb.mask = (1u << a.lut_bits) - 1u;
-    tb.lut_bits = a.lut_bits;
-    tb.max_len = a.max_len;
+    const uint32_t lane = tid & 63u;
+    const uint32_t wave = tid >> 6;
+    stage_table_blob(a, lds, tid, 64 * W);
+    const Tables tb = stage_tables(a, lds);
+    uint8_t *buf = lds + a.table_lds_bytes + wave * a.buf_bytes;
+    uint32_t *buf32 = reinterpret_cast<uint32_t *>(buf);
+    const uint32_t cap = a.buf_bytes - 8u;
+    __syncthreads();
+
+    const uint32_t first_block = blockIdx.x * W + wave;
+    const uint32_t stride = gridDim.x * W;
+    if (first_block >= a.num_blocks) return;
+    ChunkWords cw = load_chunk(a, first_block, first_block * 64u + lane);
+    Chunk ch = chunk_setup(a, cw, first_block * 64u + lane);
+    Range r = block_range(a, cw);
+
+    for (uint32_t b = first_block; b < a.num_blocks; b += stride) {
+        // loads for this block's assembly and the next block's decode
+        const uint32_t bn = b + stride;
+        ChunkWords nxt = cw;
+        if (bn < a.num_blocks) nxt = load_chunk(a, bn, bn * 64u + lane);
+        uint2 S[kPre];
+        prefetch_sm(a, r, lane, 64u, S);
+
+        wave_lds_sync();  // this wave's reads of the previous block are issued
+        for (uint32_t i = lane; i < (a.buf_bytes >> 4); i += 64u)
+            reinterpret_cast<uint4 *>(buf)[i] = make_uint4(0u, 0u, 0u, 0u);
+
+        uint32_t sy[kKeep], npk[(kKeep + 3) / 4], p_rest;
+        const uint32_t cnt = decode_count(tb, ch, sy, npk, &p_rest);
+        const uint32_t excl = wave_inclusive_scan(cnt) - cnt;
+        wave_lds_sync();
+        emit_exponents(tb, ch, sy, npk, p_rest, r.shift + excl, buf32, cap);
+        wave_lds_sync();
+
+        uint4 O[kPre];
+        assemble_prefetched(r, buf, lane, 64u, S, O);
+        const Range rb = r;
+        cw = nxt;  // next block's words: consumed before this block's stores
+        ch = chunk_setup(a, cw, bn * 64u + lane);
+        r = block_range(a, cw);
+        store_block(a, rb, buf, lane, 64u, O);
+    }
+}
+
+// T >= 128: one workgroup of T threads per block.
+template <uint32_t T>
+__global__ __launch_bounds__(T) void df11_decode_block_kernel(DecodeArgs a) {
+    extern __shared__ __align__(16) uint8_t lds[];
+    const uint32_t tid = threadIdx.x;
+    const uint32_t lane = tid & 63u;
+    const uint32_t wave = tid >> 6;
+    stage_table_blob(a, lds, tid, T);
+    const Tables tb = stage_tables(a, lds);
     uint32_t *wave_sums = reinterpret_cast<uint32_t *>(lds + a.table_lds_bytes);
     uint8_t *buf = lds + a.table_lds_bytes + 4 * kScanSlots;
     uint32_t *buf32 = reinterpret_cast<uint32_t *>(buf);
-    const uint32_t buf_dwords = a.buf_bytes >> 2;
+    const uint32_t cap = a.buf_bytes - 8u;
 
-    {  // stage the decode tables once per workgroup
-        const uint4 *src = reinterpret_cast<const uint4 *>(a.tables);
-        uint4 *dst = reinterpret_cast<uint4 *>(lds);
-        for (uint32_t i = tid; i < (a.table_lds_bytes >> 4); i += T) dst[i] = src[i];
-    }
-
-    const uint32_t lane = tid & 63u;
-    const uint32_t wave = tid >> 6;
+    if (blockIdx.x >= a.num_blocks) return;
+    ChunkWords cw = load_chunk(a, blockIdx.x, blockIdx.x * T + tid);
+    Chunk ch = chunk_setup(a, cw, blockIdx.x * T + tid);
+    Range r = block_range(a, cw);
 
     for (uint32_t b = blockIdx.x; b < a.num_blocks; b += gridDim.x) {
+        const uint32_t bn = b + gridDim.x;
+        ChunkWords nxt = cw;
+        if (bn < a.num_blocks) nxt = load_chunk(a, bn, bn * T + tid);
+        uint2 S[kPre];
+        prefetch_sm(a, r, tid, T, S);
+
         __syncthreads();  // tables staged / previous block's buffer consumed
         for (uint32_t i = tid; i < (a.buf_bytes >> 4); i += T)
             reinterpret_cast<uint4 *>(buf)[i] = make_uint4(0u, 0u, 0u, 0u);
 
-        // ---- 1. chunk bits and gaps
-        const uint32_t c = b * T + tid;
-        const uint2 own = *reinterpret_cast<const uint2 *>(a.exp + 8ull * c);
-        const uint32_t nxt = *reinterpret_cast<const uint32_t *>(a.exp + 8ull * c + 8);
-        const uint32_t w0 = lsb_first(own.x), w1 = lsb_first(own.y), w2 = lsb_first(nxt);
+        uint32_t sy[kKeep], npk[(kKeep + 3) / 4], p_rest;
+        const uint32_t cnt = decode_count(tb, ch, sy, npk, &p_rest);
 
-        const uint64_t gbit = 5ull * c;
-        const uint64_t gw = gbit >> 5;
-        const uint64_t gv = ((static_cast<uint64_t>(__builtin_bswap32(a.gaps[gw])) << 32) |
-                             __builtin_bswap32(a.gaps[gw + 1]))
-                            << (static_cast<uint32_t>(gbit) & 31u);
-        const uint32_t gap_own = static_cast<uint32_t>(gv >> 59);
-        const uint32_t gap_next = static_cast<uint32_t>(gv >> 54) & 31u;
-
-        uint32_t start = 0, end = 0;
-        if (c < a.num_chunks) {
-            start = gap_own;
-            end = (c + 1 < a.num_chunks) ? 64u + gap_next
-                                         : static_cast<uint32_t>(a.total_bits - 64ull * c);
-            end = min(end, 95u);
-        }
-
-        // ---- 2. phase 1: count the codes that start in this chunk
-        uint32_t p = start, cnt = 0, last_p = 0, last_meta = 0;
-        for (uint32_t it = 0; p < end && it < 96u; ++it) {
-            const uint2 e = lookup(tb, window_at(w0, w1, w2, p));
-            last_p = p;
-            last_meta = e.y;
-            p += e.y & 0xFFu;
-            cnt += (e.y >> 8) & 0xFFu;
-        }
-        // codes of the last lookup that start at or past `end` belong to the next chunk
-        cnt -= __builtin_popcount((last_meta >> 16) >> min(end - last_p, 31u));
-
-        // ---- 3. output positions: exclusive scan over the workgroup
         const uint32_t incl = wave_inclusive_scan(cnt);
         if (lane == 63u) wave_sums[wave] = incl;
         __syncthreads();
         uint32_t before = 0;
         for (uint32_t w = 0; w < wave; ++w) before += wave_sums[w];
-        const uint32_t excl = before + incl - cnt;
-
-        const uint32_t s = min(a.block_pos[b], a.n_elems);
-        uint32_t e_end = max(min(a.block_pos[b + 1], a.n_elems), s);
-        const uint32_t shift = s & 15u;
-        e_end = min(e_end, s + (a.buf_bytes - kBufSlack));
-        const uint32_t count = e_end - s;
-
-        // ---- 4. phase 2: exponents into the LDS buffer at their positions
-        uint32_t off = shift + excl;
-        p = start;
-        for (uint32_t it = 0; p < end && it < 96u; ++it) {
-            const uint2 e = lookup(tb, window_at(w0, w1, w2, p));
-            const uint64_t v = static_cast<uint64_t>(e.x) << ((off & 3u) * 8u);
-            const uint32_t dw = min(off >> 2, buf_dwords - 2u);
-            atomicOr(&buf32[dw], static_cast<uint32_t>(v));
-            atomicOr(&buf32[dw + 1], static_cast<uint32_t>(v >> 32));
-            off += (e.y >> 8) & 0xFFu;
-            p += e.y & 0xFFu;
-        }
+        emit_exponents(tb, ch, sy, npk, p_rest, r.shift + before + incl - cnt, buf32, cap);
         __syncthreads();
 
-        // ---- 5. assemble BF16 and write 16 outputs per lane
-        const uint32_t g0 = s - shift;
-        const uint32_t ngroups = (shift + count + 15u) >> 4;
-        for (uint32_t g = tid; g < ngroups; g += T) {
-            const uint32_t j0 = g << 4;  // buffer index of the group
-            if (j0 >= shift && j0 + 16u <= shift + count) {
-                const uint4 S = *reinterpret_cast<const uint4 *>(a.sm + g0 + j0);
-                const uint4 E = reinterpret_cast<const uint4 *>(buf)[g];
-                uint4 lo, hi;
-                assemble4(S.x, E.x, lo.x, lo.y);
-                assemble4(S.y, E.y, lo.z, lo.w);
-                assemble4(S.z, E.z, hi.x, hi.y);
-                assemble4(S.w, E.w, hi.z, hi.w);
-                uint4 *dst = reinterpret_cast<uint4 *>(a.out + g0 + j0);
-                dst[0] = lo;
-                dst[1] = hi;
-            } else {
-                for (uint32_t k = 0; k < 16u; ++k) {
-                    const uint32_t j = j0 + k;
-                    if (j >= shift && j < shift + count) {
-                        const uint32_t smb = a.sm[g0 + j];
-                        const uint32_t ex = buf[j];
-                        a.out[g0 + j] =
-                            static_cast<uint16_t>(((smb & 0x80u) << 8) | (ex << 7) | (smb & 0x7Fu));
-                    }
-                }
-            }
-        }
+        uint4 O[kPre];
+        assemble_prefetched(r, buf, tid, T, S, O);
+        const Range rb = r;
+        cw = nxt;
+        ch = chunk_setup(a, cw, bn * T + tid);
+        r = block_range(a, cw);
+        store_block(a, rb, buf, tid, T, O);
     }
 }
 
 struct DeviceInfo {
     int cus = 0;
-    int max_lds = 0;                         // bytes of LDS one workgroup may use
-    uint32_t lds_granted[5] = {0, 0, 0, 0, 0};  // dynamic LDS limit set per kernel
+    int max_lds = 0;                 // bytes of LDS one workgroup may use
+    uint32_t lds_granted[9] = {};    // dynamic LDS limit set per kernel instance
 };
 
 std::mutex g_mu;
@@ -247,15 +481,31 @@ std::vector<DeviceInfo> g_dev;
 
 using KernelFn = void (*)(DecodeArgs);
 
-KernelFn kernel_for(uint32_t T, int *slot) {
-    switch (T) {
-        case 64: *slot = 0; return df11_decode_kernel<64>;
-        case 128: *slot = 1; return df11_decode_kernel<128>;
-        case 256: *slot = 2; return df11_decode_kernel<256>;
-        case 512: *slot = 3; return df11_decode_kernel<512>;
-        case 1024: *slot = 4; return df11_decode_kernel<1024>;
+constexpr uint32_t kWaveChoices[4] = {4, 8, 12, 16};
+
+KernelFn wave_kernel(uint32_t W) {
+    switch (W) {
+        case 4: return df11_decode_wave_kernel<4>;
+        case 8: return df11_decode_wave_kernel<8>;
+        case 12: return df11_decode_wave_kernel<12>;
+        case 16: return df11_decode_wave_kernel<16>;
         default: return nullptr;
     }
+}
+
+KernelFn block_kernel(uint32_t T, int *slot) {
+    switch (T) {
+        case 128: *slot = 4; return df11_decode_block_kernel<128>;
+        case 256: *slot = 5; return df11_decode_block_kernel<256>;
+        case 512: *slot = 6; return df11_decode_block_kernel<512>;
+        case 1024: *slot = 7; return df11_decode_block_kernel<1024>;
+        default: return nullptr;
+    }
+}
+
+bool layout_supported(uint32_t T) {
+    int slot;
+    return T == 64 || block_kernel(T, &slot) != nullptr;
 }
 
 uint32_t buf_bytes_for(uint32_t max_elems) {
@@ -266,8 +516,7 @@ int check_stream(const df11_stream *s) {
     if (!s) return DF11_E_INVALID_ARG;
     const df11_sizes &z = s->sizes;
     if (s->layout.bytes_per_thread != 8) return DF11_E_UNSUPPORTED;
-    int slot;
-    if (!kernel_for(s->layout.threads_per_block, &slot)) return DF11_E_UNSUPPORTED;
+    if (!layout_supported(s->layout.threads_per_block)) return DF11_E_UNSUPPORTED;
     if (s->layout.lut_bits < 8 || s->layout.lut_bits > 12) return DF11_E_INVALID_ARG;
     if (z.n_elems == 0) return DF11_OK;
     if (!s->exp || !s->sm || !s->gaps || !s->block_pos || !s->tables) return DF11_E_INVALID_ARG;
@@ -279,6 +528,7 @@ int check_stream(const df11_stream *s) {
     if (z.gap_bytes < 4 * ((5 * (z.num_blocks * T + 1) + 31) / 32 + 2)) return DF11_E_INVALID_ARG;
     if (z.num_chunks > z.num_blocks * T) return DF11_E_INVALID_ARG;
     if (z.max_elems_per_block > 64u * T) return DF11_E_INVALID_ARG;
+    if (z.sm_bytes < ((z.n_elems + 15) & ~uint64_t{15}) + 16) return DF11_E_INVALID_ARG;
     if ((reinterpret_cast<uintptr_t>(s->sm) & 15u) || (reinterpret_cast<uintptr_t>(s->exp) & 7u) ||
         (reinterpret_cast<uintptr_t>(s->gaps) & 3u) || (reinterpret_cast<uintptr_t>(s->tables) & 15u) ||
         (reinterpret_cast<uintptr_t>(s->block_pos) & 3u))
@@ -286,13 +536,28 @@ int check_stream(const df11_stream *s) {
     return DF11_OK;
 }
 
+// Lets a kernel use `lds` bytes of dynamic LDS and returns how many of its
+// workgroups fit on one CU (0 when none does).
+int fit(DeviceInfo &di, int slot, KernelFn fn, uint32_t threads, uint32_t lds, int *per_cu) {
+    *per_cu = 0;
+    if (lds > static_cast<uint32_t>(di.max_lds)) return DF11_OK;
+    if (lds > 65536u && di.lds_granted[slot] < lds) {
+        if (hipFuncSetAttribute(reinterpret_cast<const void *>(fn),
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                static_cast<int>(lds)) != hipSuccess)
+            return DF11_E_HIP;
+        di.lds_granted[slot] = lds;
+    }
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(per_cu, reinterpret_cast<const void *>(fn),
+                                                     static_cast<int>(threads), lds) != hipSuccess)
+        return DF11_E_HIP;
+    return DF11_OK;
+}
+
 int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *block, uint32_t *lds) {
-    int slot = 0;
     const uint32_t T = s->layout.threads_per_block;
-    *fn = kernel_for(T, &slot);
     const uint32_t tab = static_cast<uint32_t>(df11tab::lds_bytes(s->layout.lut_bits));
-    *lds = tab + 4 * kScanSlots + buf_bytes_for(s->sizes.max_elems_per_block);
-    *block = T;
+    const uint32_t buf = buf_bytes_for(s->sizes.max_elems_per_block);
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return DF11_E_HIP;
     std::lock_guard<std::mutex> lk(g_mu);
@@ -304,21 +569,41 @@ int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *bloc
                 hipSuccess)
             return DF11_E_HIP;
     }
-    if (*lds > static_cast<uint32_t>(di.max_lds)) return DF11_E_UNSUPPORTED;
-    if (*lds > 65536u && di.lds_granted[slot] < *lds) {
-        if (hipFuncSetAttribute(reinterpret_cast<const void *>(*fn),
-                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                                static_cast<int>(*lds)) != hipSuccess)
-            return DF11_E_HIP;
-        di.lds_granted[slot] = *lds;
-    }
+    uint64_t blocks_needed;
     int per_cu = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(*fn),
-                                                     static_cast<int>(T), *lds) != hipSuccess)
-        return DF11_E_HIP;
-    if (per_cu < 1) return DF11_E_UNSUPPORTED;
+    if (T == 64) {
+        // most resident waves per CU; fewer waves per workgroup on a tie
+        uint32_t best_w = 0;
+        int best_waves = 0, best_per_cu = 0;
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t W = kWaveChoices[i];
+            int pc = 0;
+            int rc = fit(di, i, wave_kernel(W), 64 * W, tab + W * buf, &pc);
+            if (rc) return rc;
+            if (pc * static_cast<int>(W) > best_waves) {
+                best_waves = pc * static_cast<int>(W);
+                best_w = W;
+                best_per_cu = pc;
+            }
+        }
+        if (!best_w) return DF11_E_UNSUPPORTED;
+        *fn = wave_kernel(best_w);
+        *block = 64 * best_w;
+        *lds = tab + best_w * buf;
+        per_cu = best_per_cu;
+        blocks_needed = (s->sizes.num_blocks + best_w - 1) / best_w;
+    } else {
+        int slot = 0;
+        *fn = block_kernel(T, &slot);
+        *block = T;
+        *lds = tab + 4 * kScanSlots + buf;
+        int rc = fit(di, slot, *fn, T, *lds, &per_cu);
+        if (rc) return rc;
+        if (per_cu < 1) return DF11_E_UNSUPPORTED;
+        blocks_needed = s->sizes.num_blocks;
+    }
     uint64_t g = static_cast<uint64_t>(di.cus) * static_cast<uint64_t>(per_cu);
-    if (g > s->sizes.num_blocks) g = s->sizes.num_blocks;
+    if (g > blocks_needed) g = blocks_needed;
     *grid = static_cast<uint32_t>(g ? g : 1);
     return DF11_OK;
 }

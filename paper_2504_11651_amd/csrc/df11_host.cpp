@@ -275,7 +275,7 @@ int df11_encoded_sizes(const df11_codebook *cb, const df11_layout *lay, df11_siz
     out->num_chunks = ceil_div(bits, 8 * n_bytes);
     out->num_blocks = ceil_div(out->num_chunks, T);
     out->exp_bytes = out->num_blocks * n_bytes * T + 16;
-    out->sm_bytes = n;
+    out->sm_bytes = ((n + 15) & ~uint64_t{15}) + 16;  // zero padded for 16-byte reads
     out->gap_bytes = 4 * (ceil_div(5 * (out->num_blocks * T + 1), 32) + 2);
     out->block_pos_bytes = 4 * (out->num_blocks + 1);
     out->table_bytes = df11tab::blob_bytes(lay->lut_bits);
@@ -286,7 +286,7 @@ int df11_encoded_sizes(const df11_codebook *cb, const df11_layout *lay, df11_siz
 int df11_encode(const uint16_t *bf16, uint64_t n, const df11_codebook *cb, const df11_layout *lay,
                 uint8_t *exp, uint64_t exp_cap, uint8_t *sm, uint64_t sm_cap, uint8_t *gaps,
                 uint64_t gap_cap, uint32_t *block_pos, uint64_t block_pos_cap, df11_sizes *out) {
-    if ((n && (!bf16 || !sm)) || !cb || !exp || !gaps || !block_pos || !out)
+    if ((n && !bf16) || !sm || !cb || !exp || !gaps || !block_pos || !out)
         return DF11_E_INVALID_ARG;
     df11_sizes sz;
     int rc = df11_encoded_sizes(cb, lay, &sz);
@@ -384,6 +384,7 @@ int df11_encode(const uint16_t *bf16, uint64_t n, const df11_codebook *cb, const
             }
         }
     });
+    std::memset(sm + n, 0, sz.sm_bytes - n);
     for (unsigned p = 0; p < parts; ++p) {
         uint64_t lo = n * p / parts, hi = n * (p + 1) / parts;
         if (lo >= hi) continue;
@@ -438,7 +439,8 @@ int df11_validate(const df11_stream *s) {
         return DF11_E_INVALID_ARG;
     const uint64_t n_bytes = s->layout.bytes_per_thread, T = s->layout.threads_per_block;
     if (z.max_code_len > 32 || z.max_code_len > 8 * n_bytes) return DF11_E_CORRUPT;
-    if (z.n_elems > 0xFFFFFFFFull || z.sm_bytes != z.n_elems) return DF11_E_CORRUPT;
+    if (z.n_elems > 0xFFFFFFFFull || z.sm_bytes != ((z.n_elems + 15) & ~uint64_t{15}) + 16)
+        return DF11_E_CORRUPT;
     if (z.num_chunks != ceil_div(z.total_bits, 8 * n_bytes)) return DF11_E_CORRUPT;
     if (z.num_blocks != ceil_div(z.num_chunks, T)) return DF11_E_CORRUPT;
     if (z.exp_bytes != z.num_blocks * n_bytes * T + 16) return DF11_E_CORRUPT;

@@ -46,7 +46,8 @@ def test_stream_identical_to_oracle(case, lay):
     assert hs.sizes.total_bits == st["total_bits"]
     assert hs.sizes.num_chunks == st["num_chunks"] and hs.sizes.num_blocks == st["num_blocks"]
     assert np.array_equal(hs.exp, st["exp"])
-    assert np.array_equal(hs.sm, st["sm"])
+    assert np.array_equal(hs.sm[:w.size], st["sm"])
+    assert hs.sm.size == ((w.size + 15) // 16) * 16 + 16 and not hs.sm[w.size:].any()
     assert np.array_equal(hs.gaps, st["gaps_packed"])
     assert np.array_equal(hs.block_pos, st["block_pos"])
     bp = st["block_pos"].astype(np.int64)
@@ -227,7 +228,7 @@ def kernel_model_decode(hs: codec.HostStream) -> np.ndarray:
                 p += meta & 0xFF
     n = int(z.n_elems)
     e = np.array([out_exp[i] for i in range(n)], np.uint16)
-    sm = hs.sm.astype(np.uint16)
+    sm = hs.sm[:n].astype(np.uint16)
     return ((sm & 0x80) << 8) | (e << 7) | (sm & 0x7F)
 
 
