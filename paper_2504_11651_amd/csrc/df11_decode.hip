@@ -317,7 +317,7 @@ __device__ __forceinline__ uint4 assemble_group(const uint8_t *buf, uint32_t g, 
 }
 
 // One 16-byte store, or single-element stores for the elements of a group
-// that the block shares with its neighbour.
+// that the block shares with its neighbour (elements k in [lo, hi)).
 __device__ __forceinline__ void store_group(const DecodeArgs &a, const Range &r, uint32_t g,
                                             const uint4 &o) {
     uint16_t *dst = a.out + r.g0 + (g << 3);
@@ -325,33 +325,29 @@ __device__ __forceinline__ void store_group(const DecodeArgs &a, const Range &r,
         *reinterpret_cast<uint4 *>(dst) = o;
         return;
     }
+    const int lo = static_cast<int>(r.shift) - static_cast<int>(g << 3);
+    const int hi = static_cast<int>(r.lim) - static_cast<int>(g << 3);
     const uint32_t v[4] = {o.x, o.y, o.z, o.w};
 #pragma unroll
-    for (uint32_t k = 0; k < 8u; ++k) {
-        const uint32_t j = (g << 3) + k;
-        if (j >= r.shift && j < r.lim) dst[k] = static_cast<uint16_t>(v[k >> 1] >> ((k & 1u) * 16u));
-    }
+    for (int k = 0; k < 8; ++k)
+        if (k >= lo && k < hi) dst[k] = static_cast<uint16_t>(v[k >> 1] >> ((k & 1) * 16));
 }
 
-// Outputs of the prefetched groups first + k*step (k < kPre).  Loads and
-// stores share one counter on this GPU, and a wait for a load issued before a
-// pending store has to wait for the store as well; so every prefetched value
-// is consumed here, before any store of the block is issued.
-__device__ __forceinline__ void assemble_prefetched(const Range &r, const uint8_t *buf,
-                                                    uint32_t first, uint32_t step,
-                                                    const uint2 (&S)[kPre], uint4 (&O)[kPre]) {
+// Assemble and store every group of the block: groups first + k*step.  The
+// first kPre use the bytes fetched when the block started.  Loads and stores
+// share one in-order counter on this GPU, so all of those groups are
+// assembled (their loads waited for) before the first store is issued;
+// otherwise each wait would also wait for the stores issued before it.
+__device__ __forceinline__ void assemble_block(const DecodeArgs &a, const Range &r,
+                                               const uint8_t *buf, uint32_t first, uint32_t step,
+                                               const uint2 (&S)[kPre]) {
+    uint4 O[kPre];
 #pragma unroll
     for (int k = 0; k < kPre; ++k) {
         const uint32_t g = first + k * step;
         O[k] = make_uint4(0u, 0u, 0u, 0u);
         if (g < r.ngroups) O[k] = assemble_group(buf, g, S[k]);
     }
-}
-
-// Stores of the prefetched groups, then the groups past them (a block with
-// more than kPre groups per lane reads their bytes here).
-__device__ __forceinline__ void store_block(const DecodeArgs &a, const Range &r, const uint8_t *buf,
-                                            uint32_t first, uint32_t step, const uint4 (&O)[kPre]) {
 #pragma unroll
     for (int k = 0; k < kPre; ++k) {
         const uint32_t g = first + k * step;
@@ -409,13 +405,10 @@ __global__ __launch_bounds__(64 * W) void df11_decode_wave_kernel(DecodeArgs a) 
         emit_exponents(tb, ch, sy, npk, p_rest, r.shift + excl, buf32, cap);
         wave_lds_sync();
 
-        uint4 O[kPre];
-        assemble_prefetched(r, buf, lane, 64u, S, O);
-        const Range rb = r;
-        cw = nxt;  // next block's words: consumed before this block's stores
+        assemble_block(a, r, buf, lane, 64u, S);
+        cw = nxt;
         ch = chunk_setup(a, cw, bn * 64u + lane);
         r = block_range(a, cw);
-        store_block(a, rb, buf, lane, 64u, O);
     }
 }
 
@@ -460,13 +453,10 @@ __global__ __launch_bounds__(T) void df11_decode_block_kernel(DecodeArgs a) {
         emit_exponents(tb, ch, sy, npk, p_rest, r.shift + before + incl - cnt, buf32, cap);
         __syncthreads();
 
-        uint4 O[kPre];
-        assemble_prefetched(r, buf, tid, T, S, O);
-        const Range rb = r;
+        assemble_block(a, r, buf, tid, T, S);
         cw = nxt;
         ch = chunk_setup(a, cw, bn * T + tid);
         r = block_range(a, cw);
-        store_block(a, rb, buf, tid, T, O);
     }
 }
 
