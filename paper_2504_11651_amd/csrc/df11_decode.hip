@@ -39,7 +39,10 @@
 namespace {
 
 constexpr uint32_t kScanSlots = 16;  // waves per workgroup (<= 1024 threads)
-constexpr uint32_t kBufSlack = 32;   // alignment shift (< 8) + over-decoded bytes
+// Exponent buffer bytes past the largest block: alignment shift (< 8), codes
+// decoded past a block's end, and the 4 bytes per kept lookup that a lane may
+// store past a clamped start offset.
+constexpr uint32_t kBufSlack = 128;
 
 struct DecodeArgs {
     const uint8_t *exp;
@@ -58,6 +61,9 @@ struct DecodeArgs {
     uint32_t buf_bytes;        // exponent buffer, multiple of 16
 };
 
+__device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b ? a : b; }
+__device__ __forceinline__ uint32_t umax(uint32_t a, uint32_t b) { return a > b ? a : b; }
+
 // 4 stream bytes as loaded (little endian) -> word whose bit j is stream bit j
 // (the stream is most-significant-bit first within each byte).
 __device__ __forceinline__ uint32_t lsb_first(uint32_t le) {
@@ -72,8 +78,17 @@ __device__ __forceinline__ uint32_t window_at(uint32_t w0, uint32_t w1, uint32_t
     return __builtin_amdgcn_alignbit(hi, lo, p);
 }
 
+// The kernels declare no static LDS, so the dynamically sized LDS (and the
+// decode table at its start) begins at group-segment offset 0; table entries
+// are read through LDS byte offsets.
+__device__ __forceinline__ uint2 lds_entry(uint32_t byte_offset) {
+    const uint64_t v = *(__attribute__((address_space(3))) const uint64_t *)
+        static_cast<uintptr_t>(byte_offset);
+    return make_uint2(static_cast<uint32_t>(v), static_cast<uint32_t>(v >> 32));
+}
+
 struct Tables {
-    const uint8_t *ent;      // K-bit entries, 8 bytes: x = exponents, y = meta
+    // K-bit entries (8 bytes: x = exponents, y = meta) at LDS offset 0
     const uint32_t *lj_last; // [33]
     const uint32_t *offset;  // [33]
     const uint8_t *sorted;   // [256]
@@ -85,7 +100,6 @@ struct Tables {
 __device__ __forceinline__ Tables stage_tables(const DecodeArgs &a, uint8_t *lds) {
     Tables tb;
     const uint32_t ent_bytes = 8u << a.lut_bits;
-    tb.ent = lds;
     tb.lj_last = reinterpret_cast<const uint32_t *>(lds + ent_bytes);
     tb.offset = tb.lj_last + 33;
     tb.sorted = reinterpret_cast<const uint8_t *>(tb.offset + 33);
@@ -195,7 +209,7 @@ __device__ __forceinline__ Chunk chunk_setup(const DecodeArgs &a, const ChunkWor
 
 __device__ __forceinline__ uint2 lookup(const Tables &t, const Chunk &ch, uint32_t p) {
     const uint32_t ws = window_at(ch.s0, ch.s1, ch.s2, p);
-    uint2 e = *reinterpret_cast<const uint2 *>(t.ent + (ws & t.addr_mask));
+    uint2 e = lds_entry(ws & t.addr_mask);
     if (e.y == 0u) e = decode_long(t, window_at(ch.w0, ch.w1, ch.w2, p));
     return e;
 }
@@ -216,7 +230,7 @@ __device__ __forceinline__ uint32_t decode_count(const Tables &t, const Chunk &c
         sy[k] = 0u;
         if (__builtin_amdgcn_ballot_w64(act) == 0) continue;  // wave-uniform skip
         const uint32_t ws = window_at(ch.s0, ch.s1, ch.s2, p);
-        uint2 e = *reinterpret_cast<const uint2 *>(t.ent + (ws & t.addr_mask));
+        uint2 e = lds_entry(ws & t.addr_mask);
         if (act && e.y == 0u) e = decode_long(t, window_at(ch.w0, ch.w1, ch.w2, p));
         const uint32_t m = act ? e.y : 0u;
         sy[k] = e.x;
@@ -240,34 +254,36 @@ __device__ __forceinline__ uint32_t decode_count(const Tables &t, const Chunk &c
 }
 
 // OR 4 exponent bytes into the zeroed buffer at byte offset off.
-__device__ __forceinline__ void or_exponents(uint32_t *buf32, uint32_t cap_bytes, uint32_t off,
-                                             uint32_t syms) {
+__device__ __forceinline__ void or_exponents(uint32_t *buf32, uint32_t off, uint32_t syms) {
     const uint64_t v = static_cast<uint64_t>(syms) << ((off & 3u) << 3);
-    const uint32_t dw = min(off, cap_bytes) >> 2;
-    atomicOr(&buf32[dw], static_cast<uint32_t>(v));
-    atomicOr(&buf32[dw + 1], static_cast<uint32_t>(v >> 32));
+    atomicOr(&buf32[off >> 2], static_cast<uint32_t>(v));
+    atomicOr(&buf32[(off >> 2) + 1], static_cast<uint32_t>(v >> 32));
 }
 
 // Phase 2: exponents into the LDS buffer at output offset off (the kept
-// lookups, then the rest of a long chunk by decoding again).
+// lookups, then the rest of a long chunk by decoding again).  A valid entry
+// holds at most 4 codes, so 3 bits of each kept count suffice; with the start
+// clamped, the kept lookups stay inside the buffer whatever the metadata and
+// tables hold; the rest are clamped one by one.
 __device__ __forceinline__ void emit_exponents(const Tables &t, const Chunk &ch,
                                                const uint32_t (&sy)[kKeep],
                                                const uint32_t (&npk)[(kKeep + 3) / 4],
                                                uint32_t p_rest, uint32_t off, uint32_t *buf32,
                                                uint32_t cap_bytes) {
+    off = umin(off, cap_bytes - 8u * kKeep);
 #pragma unroll
     for (int k = 0; k < kKeep; ++k) {
-        const uint32_t n = (npk[k / 4] >> (8 * (k % 4))) & 0xFFu;
-        if (__builtin_amdgcn_ballot_w64(n != 0u) == 0) continue;
+        const uint32_t n = (npk[k / 4] >> (8 * (k % 4))) & 7u;
         if (n != 0u) {
-            or_exponents(buf32, cap_bytes, off, sy[k]);
+            or_exponents(buf32, off, sy[k]);
             off += n;
         }
     }
     uint32_t p = p_rest;
     for (uint32_t it = 0; p < ch.end && it < 96u; ++it) {
         const uint2 e = lookup(t, ch, p);
-        or_exponents(buf32, cap_bytes, off, e.x);
+        off = umin(off, cap_bytes);
+        or_exponents(buf32, off, e.x);
         off += (e.y >> 8) & 0xFFu;
         p += e.y & 0xFFu;
     }
@@ -280,9 +296,9 @@ struct Range {
 
 __device__ __forceinline__ Range block_range(const DecodeArgs &a, const ChunkWords &cw) {
     Range r;
-    r.s = min(__builtin_amdgcn_readfirstlane(cw.bp0), a.n_elems);
-    uint32_t e = max(min(__builtin_amdgcn_readfirstlane(cw.bp1), a.n_elems), r.s);
-    e = min(e, r.s + (a.buf_bytes - kBufSlack));
+    r.s = umin(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(cw.bp0)), a.n_elems);
+    uint32_t e = umax(umin(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(cw.bp1)), a.n_elems), r.s);
+    e = umin(e, r.s + (a.buf_bytes - kBufSlack));
     r.shift = r.s & 7u;
     r.lim = r.shift + (e - r.s);
     r.g0 = r.s - r.shift;
@@ -299,10 +315,10 @@ __device__ __forceinline__ bool full_group(const Range &r, uint32_t g) {
 // group can be read even where the block starts or ends inside it.
 __device__ __forceinline__ void prefetch_sm(const DecodeArgs &a, const Range &r, uint32_t first,
                                             uint32_t step, uint2 (&S)[kPre]) {
-    const uint32_t last = max(r.ngroups, 1u) - 1u;  // groups past the block reread its last one
+    const uint32_t last = umax(r.ngroups, 1u) - 1u;  // groups past the block reread its last one
 #pragma unroll
     for (int k = 0; k < kPre; ++k) {
-        const uint32_t g = min(first + k * step, last);
+        const uint32_t g = umin(first + k * step, last);
         S[k] = *reinterpret_cast<const uint2 *>(a.sm + r.g0 + (g << 3));
     }
 }
@@ -316,13 +332,16 @@ __device__ __forceinline__ uint4 assemble_group(const uint8_t *buf, uint32_t g, 
     return o;
 }
 
-// One 16-byte store, or single-element stores for the elements of a group
+// One 16-byte non-temporal store (the output is written once and not read
+// back by this kernel), or single-element stores for the elements of a group
 // that the block shares with its neighbour (elements k in [lo, hi)).
 __device__ __forceinline__ void store_group(const DecodeArgs &a, const Range &r, uint32_t g,
                                             const uint4 &o) {
     uint16_t *dst = a.out + r.g0 + (g << 3);
     if (full_group(r, g)) {
-        *reinterpret_cast<uint4 *>(dst) = o;
+        typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4 ov = {o.x, o.y, o.z, o.w};
+        __builtin_nontemporal_store(ov, reinterpret_cast<u32x4 *>(dst));
         return;
     }
     const int lo = static_cast<int>(r.shift) - static_cast<int>(g << 3);
