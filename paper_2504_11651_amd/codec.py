@@ -71,7 +71,7 @@ class Stream(ctypes.Structure):
                 ("layout", Layout)]
 
 
-DEFAULT_LAYOUT = (8, 64, 12)  # bytes per thread, threads per block, table index bits
+DEFAULT_LAYOUT = (8, 64, 11)  # bytes per thread, threads per block, table index bits
 
 _lib = None
 

@@ -479,16 +479,23 @@ __global__ __launch_bounds__(T) void df11_decode_block_kernel(DecodeArgs a) {
     }
 }
 
+using KernelFn = void (*)(DecodeArgs);
+
+struct LaunchShape {
+    uint32_t threads, lut_bits, buf;  // key
+    KernelFn fn;
+    uint32_t block, lds, per_cu, waves_per_group;
+};
+
 struct DeviceInfo {
     int cus = 0;
     int max_lds = 0;                 // bytes of LDS one workgroup may use
     uint32_t lds_granted[9] = {};    // dynamic LDS limit set per kernel instance
+    std::vector<LaunchShape> shapes; // launch shapes already worked out
 };
 
 std::mutex g_mu;
 std::vector<DeviceInfo> g_dev;
-
-using KernelFn = void (*)(DecodeArgs);
 
 constexpr uint32_t kWaveChoices[4] = {4, 8, 12, 16};
 
@@ -565,7 +572,8 @@ int fit(DeviceInfo &di, int slot, KernelFn fn, uint32_t threads, uint32_t lds, i
 
 int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *block, uint32_t *lds) {
     const uint32_t T = s->layout.threads_per_block;
-    const uint32_t tab = static_cast<uint32_t>(df11tab::lds_bytes(s->layout.lut_bits));
+    const uint32_t K = s->layout.lut_bits;
+    const uint32_t tab = static_cast<uint32_t>(df11tab::lds_bytes(K));
     const uint32_t buf = buf_bytes_for(s->sizes.max_elems_per_block);
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return DF11_E_HIP;
@@ -578,40 +586,48 @@ int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *bloc
                 hipSuccess)
             return DF11_E_HIP;
     }
-    uint64_t blocks_needed;
-    int per_cu = 0;
-    if (T == 64) {
-        // most resident waves per CU; fewer waves per workgroup on a tie
-        uint32_t best_w = 0;
-        int best_waves = 0, best_per_cu = 0;
-        for (int i = 0; i < 4; ++i) {
-            const uint32_t W = kWaveChoices[i];
-            int pc = 0;
-            int rc = fit(di, i, wave_kernel(W), 64 * W, tab + W * buf, &pc);
-            if (rc) return rc;
-            if (pc * static_cast<int>(W) > best_waves) {
-                best_waves = pc * static_cast<int>(W);
-                best_w = W;
-                best_per_cu = pc;
+    const LaunchShape *found = nullptr;
+    for (const LaunchShape &ls : di.shapes)
+        if (ls.threads == T && ls.lut_bits == K && ls.buf == buf) found = &ls;
+    if (!found) {
+        LaunchShape ls{T, K, buf, nullptr, 0, 0, 0, 1};
+        if (T == 64) {
+            // most resident waves per CU; fewer waves per workgroup on a tie
+            int best_waves = 0;
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t W = kWaveChoices[i];
+                int pc = 0;
+                int rc = fit(di, i, wave_kernel(W), 64 * W, tab + W * buf, &pc);
+                if (rc) return rc;
+                if (pc * static_cast<int>(W) > best_waves) {
+                    best_waves = pc * static_cast<int>(W);
+                    ls.fn = wave_kernel(W);
+                    ls.block = 64 * W;
+                    ls.lds = tab + W * buf;
+                    ls.per_cu = static_cast<uint32_t>(pc);
+                    ls.waves_per_group = W;
+                }
             }
+            if (!best_waves) return DF11_E_UNSUPPORTED;
+        } else {
+            int slot = 0, pc = 0;
+            ls.fn = block_kernel(T, &slot);
+            ls.block = T;
+            ls.lds = tab + 4 * kScanSlots + buf;
+            int rc = fit(di, slot, ls.fn, T, ls.lds, &pc);
+            if (rc) return rc;
+            if (pc < 1) return DF11_E_UNSUPPORTED;
+            ls.per_cu = static_cast<uint32_t>(pc);
         }
-        if (!best_w) return DF11_E_UNSUPPORTED;
-        *fn = wave_kernel(best_w);
-        *block = 64 * best_w;
-        *lds = tab + best_w * buf;
-        per_cu = best_per_cu;
-        blocks_needed = (s->sizes.num_blocks + best_w - 1) / best_w;
-    } else {
-        int slot = 0;
-        *fn = block_kernel(T, &slot);
-        *block = T;
-        *lds = tab + 4 * kScanSlots + buf;
-        int rc = fit(di, slot, *fn, T, *lds, &per_cu);
-        if (rc) return rc;
-        if (per_cu < 1) return DF11_E_UNSUPPORTED;
-        blocks_needed = s->sizes.num_blocks;
+        di.shapes.push_back(ls);
+        found = &di.shapes.back();
     }
-    uint64_t g = static_cast<uint64_t>(di.cus) * static_cast<uint64_t>(per_cu);
+    *fn = found->fn;
+    *block = found->block;
+    *lds = found->lds;
+    const uint64_t W = found->waves_per_group;
+    const uint64_t blocks_needed = (s->sizes.num_blocks + W - 1) / W;
+    uint64_t g = static_cast<uint64_t>(di.cus) * found->per_cu;
     if (g > blocks_needed) g = blocks_needed;
     *grid = static_cast<uint32_t>(g ? g : 1);
     return DF11_OK;
