@@ -49,7 +49,40 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def cpu_baseline(hs, w, min_seconds: float = 10.0, max_reps: int = 4) -> dict:
+DECODER_SOURCES = ("paper_2504_11651_amd/csrc/df11_decode.hip",
+                   "paper_2504_11651_amd/csrc/df11_tables.h")
+
+
+def profiled_traffic(workload_name: str, lay) -> float | None:
+    """HBM bytes per launch from the committed rocprofv3 counter summary of this
+    workload and layout: FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
+    scaled by what the same counter reads for a 512 MiB copy.  None when no
+    summary exists or the decoder source changed since it was taken."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for p in DECODER_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    want = {"workload": workload_name, "source_sha256": h.hexdigest(),
+            "layout": f"{lay.bytes_per_thread},{lay.threads_per_block},{lay.lut_bits}"}
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*_counters.md"))):
+        kv = {}
+        with open(path) as f:
+            for line in f:
+                k, sep, v = line.strip().partition(": ")
+                if sep and k.replace("_", "").isalnum():
+                    kv[k] = v.strip()
+        if all(kv.get(k) == v for k, v in want.items()):
+            try:
+                return 1024.0 * (float(kv["fetch_kib_per_launch"]) * float(kv["fetch_scale"]) +
+                                 float(kv["write_kib_per_launch"]) * float(kv["write_scale"]))
+            except (KeyError, ValueError):
+                return None
+    return None
+
+
+def cpu_baseline(hs, w, min_seconds: float = 10.0, max_reps: int = 16) -> dict:
     """The oracle's bit-serial decode of the same stream on one host core."""
     import oracle
     n = w.size
@@ -178,6 +211,7 @@ def main() -> int:
     ms_per_step = wall * 1e3 / args.steps
     value = 2.0 * n / (ms_per_step * 1e-3) / 1e9
     grid, block, lds = codec.launch_shape(ds)
+    traffic = profiled_traffic(args.workload, lay)
 
     rec = {
         "metric": METRIC,
@@ -207,7 +241,7 @@ def main() -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": None if traffic is None else round(traffic),
         },
         "pct_hbm_roofline": round(100.0 * achieved / HBM_PEAK_GBS, 2),
         "weights_per_s": round(n / (ms_per_step * 1e-3), 1),
