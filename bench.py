@@ -6,7 +6,11 @@ resident in HBM, into a reused BF16 workspace -- the whole decode path in
 one launch.  Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                  [--no-cpu-baseline] [--calib] [--cold]
+                  [--tokens T] [--no-cpu-baseline] [--calib] [--cold]
+
+--workload llama3_8b_stack times the decode-then-products driver instead: 32
+blocks resident in compressed form, one step = decode one block into a reused
+workspace plus its 7 products at T activation rows.
 """
 from __future__ import annotations
 
@@ -37,6 +41,110 @@ def workload(name: str):
     if name == "matrix_4096":
         return synth.matrix_4096()
     raise SystemExit(f"unknown workload {name}")
+
+
+def stack_mats():
+    from paper_2504_11651_amd import synth
+    mats, off = [], 0
+    for _, r, c in synth.LLAMA3_8B_BLOCK:
+        mats.append((off, r, c))
+        off += r * c
+    return mats, off
+
+
+def run_stack(args) -> int:
+    """32 Llama-3-8B-shaped blocks kept compressed on the device; one step =
+    decode block (step mod 32) into a reused BF16 workspace, then its 7
+    products at --tokens activation rows (MFMA, fp32 accumulation)."""
+    import torch
+    from paper_2504_11651_amd import codec, synth
+    dev = torch.device("cuda:0")
+    blocks = 32
+    mats, n = stack_mats()
+    t0 = time.perf_counter()
+    streams, comp_bytes, w0 = [], [], None
+    for i in range(blocks):
+        w, _ = synth.llama3_8b_stack_block(i)
+        hs = codec.encode(w)
+        z = hs.sizes
+        comp_bytes.append((int(z.total_bits) + 7) // 8 + n + int(z.gap_bytes) +
+                          int(z.block_pos_bytes) + int(z.table_bytes))
+        streams.append(codec.to_device(hs, dev))
+        if i == 0:
+            w0 = w
+    t_prep = time.perf_counter() - t0
+    T = args.tokens
+    x1 = torch.from_numpy(synth.activations(T, 4096, 5, 0, 1).view(np.int16)).to(dev)
+    x2 = torch.from_numpy(synth.activations(T, 14336, 5, 0, 2).view(np.int16)).to(dev)
+    xs = [x1.view(torch.bfloat16)] * 6 + [x2.view(torch.bfloat16)]
+    ys = [torch.empty((T, r), dtype=torch.float32, device=dev) for _, r, _ in mats]
+    ws = torch.empty(max(codec.gemm_workspace_bytes(mats, T) // 4, 1), dtype=torch.float32,
+                     device=dev)
+    work = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    # bit-exact decode and bit-identical products before timing (block 0)
+    codec.block_forward(streams[0], work, mats, xs, ys, ws, stream=stream)
+    y_ref = [torch.empty_like(y) for y in ys]
+    raw = torch.from_numpy(w0.view(np.int16)).to(dev)
+    codec.block_gemm(raw.view(torch.bfloat16), mats, xs, y_ref, ws, stream=stream)
+    torch.cuda.synchronize()
+    bit_exact = bool(torch.equal(work.view(torch.int16), raw)) and all(
+        torch.equal(a.view(torch.int32), b.view(torch.int32)) for a, b in zip(ys, y_ref))
+    assert bit_exact, "decode or products differ from the uncompressed weights"
+    del raw, y_ref
+
+    def timed(fn, steps):
+        for i in range(args.warmup):
+            fn(i)
+        torch.cuda.synchronize()
+        s_ev, e_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t_0 = time.perf_counter()
+        s_ev.record(stream)
+        for i in range(steps):
+            fn(i)
+        e_ev.record(stream)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t_0) * 1e3 / steps, s_ev.elapsed_time(e_ev) / steps
+
+    step = lambda i: codec.block_forward(streams[i % blocks], work, mats, xs, ys, ws,
+                                         stream=stream)
+    dec = lambda i: codec.decode_block(streams[i % blocks], work, stream=stream)
+    gemm = lambda i: codec.block_gemm(work, mats, xs, ys, ws, stream=stream)
+    wall_ms, step_ms = timed(step, args.steps)
+    _, dec_ms = timed(dec, args.steps)
+    _, gemm_ms = timed(gemm, args.steps)
+
+    mean_comp = float(np.mean(comp_bytes))
+    x_bytes = 2 * T * (6 * 4096 + 14336)
+    y_bytes = 4 * T * sum(r for _, r, _ in mats)
+    dec_bytes = mean_comp + 2 * n
+    gemm_bytes = 2 * n + x_bytes + y_bytes
+    achieved = dec_bytes / (dec_ms * 1e-3) / 1e9
+    rec = {
+        "metric": METRIC,
+        "value": round(2.0 * n / (wall_ms * 1e-3) / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall_ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "u32+bf16", "data": "synthetic",
+        "config": {"workload": "llama3_8b_stack", "blocks": blocks, "weights_per_block": n,
+                   "tokens": T, "step": "decode block (step mod 32) + 7 products (MFMA bf16, "
+                                        "fp32 accumulate)"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": None, "kernel": "decode"},
+        "bit_exact": bit_exact,
+        "kernel_ms": {"step_in_timed_region": round(step_ms, 5), "decode": round(dec_ms, 5),
+                      "products": round(gemm_ms, 5)},
+        "products_gbs": round(gemm_bytes / (gemm_ms * 1e-3) / 1e9, 1),
+        "tokens_per_s_per_block": round(T / (wall_ms * 1e-3), 1),
+        "compressed_bytes_resident": int(sum(comp_bytes)),
+        "host_s": {"generate_and_encode": round(t_prep, 2)},
+    }
+    print(json.dumps(rec), flush=True)
+    return 0
 
 
 def cpu_model() -> str:
@@ -107,7 +215,10 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=500)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default="llama3_8b_block")
+    ap.add_argument("--workload", default="llama3_8b_block",
+                    help="llama3_8b_block, heavy_tailed_block, llama31_70b_block, matrix_4096, "
+                         "llama3_8b_stack (decode + 7 products per step)")
+    ap.add_argument("--tokens", type=int, default=64, help="activation rows (llama3_8b_stack)")
     ap.add_argument("--threads", type=int, default=None, help="threads per block T")
     ap.add_argument("--lut-bits", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -126,6 +237,8 @@ def main() -> int:
     from paper_2504_11651_amd import codec
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.workload == "llama3_8b_stack":
+        return run_stack(args)
     dev = torch.device("cuda:0")
     t0 = time.perf_counter()
     w = workload(args.workload)

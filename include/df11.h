@@ -38,9 +38,10 @@
  *     built from the code book by df11_build_tables; it is opaque to callers.
  *
  * Memory ownership: the caller allocates and frees every buffer.  Host
- * functions take host pointers; df11_decode_block takes device pointers
- * (inside df11_stream) and a device output pointer.  The library keeps no
- * per-call state and allocates no device memory on the decode path.
+ * functions take host pointers; df11_decode_block, df11_block_gemm and
+ * df11_block_forward take device pointers (inside df11_stream, and for the
+ * weights, activations, outputs and workspace).  The library keeps no
+ * per-call state and allocates no device memory.
  *
  * Errors: every function returns DF11_OK (0) or a negative DF11_E_* code;
  * nothing is thrown across the ABI.  df11_strerror names a code.
@@ -144,19 +145,75 @@ int df11_build_tables(const df11_codebook *cb, uint32_t lut_bits, uint8_t *table
 int df11_validate(const df11_stream *host_view);
 
 /* Decompress one stream into n_elems BF16 values at out (device memory,
- * 2*n_elems bytes, 2-byte aligned) -- the whole of Algorithm 1 on the GPU.
+ * 2*n_elems bytes, 16-byte aligned) -- the whole of Algorithm 1 on the GPU.
  * All stream pointers are device pointers.  One transformer block encoded
  * as one stream decodes in one launch (Sec. 2.3.3).  The work is enqueued
  * on `stream` and the call returns without waiting; buffers must stay alive
  * until the stream has executed it.  n_elems == 0 launches nothing.
- * Returns DF11_E_UNSUPPORTED for bytes_per_thread != 8, DF11_E_HIP when the
- * launch fails. */
+ * Returns DF11_E_UNSUPPORTED for bytes_per_thread != 8, DF11_E_INVALID_ARG for
+ * a null or misaligned pointer (exp 8-byte, sm and tables 16-byte, gaps and
+ * block_pos 4-byte aligned) or inconsistent sizes, DF11_E_HIP when the launch
+ * fails. */
 int df11_decode_block(const df11_stream *dev, uint16_t *out, hipStream_t stream);
 
 /* Launch shape df11_decode_block would use on the current device for this
  * stream: workgroups, threads per workgroup and LDS bytes per workgroup. */
 int df11_decode_launch_shape(const df11_stream *dev, uint32_t *grid, uint32_t *block,
                              uint32_t *lds_bytes);
+
+/* ---- Decode-then-GEMM block driver (Sec. 2.3.3 and the batch-size
+ * experiments of Sec. 3: a transformer block is decompressed into a BF16
+ * workspace right before its matrix multiplications, and the decoded
+ * weights are discarded afterwards). */
+
+#define DF11_MAX_MATRICES 8 /* matrices per block call */
+#define DF11_MAX_TOKENS 64  /* activation rows per call */
+
+/* One weight matrix inside a block of BF16 weights: rows x cols, row-major
+ * ([out features, in features]), starting `offset` weights into the block.
+ * Requirements: rows a multiple of 16, cols a multiple of 64, offset a
+ * multiple of 8 (16-byte aligned rows). */
+typedef struct {
+    uint64_t offset;
+    uint32_t rows;
+    uint32_t cols;
+} df11_matrix;
+
+/* Device workspace bytes df11_block_gemm / df11_block_forward need for these
+ * matrices at this many tokens (partial sums of matrices whose cols are
+ * split across workgroups; 0 when none is).  Host, no device access. */
+int df11_gemm_workspace_bytes(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens,
+                              uint64_t *bytes);
+
+/* For every matrix m: y[m] = x[m] * W_m^T, i.e.
+ *   y[m][t][r] = sum_k x[m][t][k] * W_m[r][k],
+ * BF16 products accumulated in fp32 on the matrix cores, fp32 output.
+ *   weights:   device, n_weights BF16 values (the block);
+ *   mats:      host array of n_mats (1..DF11_MAX_MATRICES) descriptors, each
+ *              inside [0, n_weights);
+ *   x:         host array of n_mats device pointers, x[m] is tokens x cols_m
+ *              BF16 row-major, 16-byte aligned;
+ *   y:         host array of n_mats device pointers, y[m] is tokens x rows_m
+ *              fp32 row-major, 4-byte aligned;
+ *   tokens:    1..DF11_MAX_TOKENS;
+ *   workspace: device, at least df11_gemm_workspace_bytes (may be null when
+ *              that is 0), 16-byte aligned.
+ * The result depends only on the inputs and shapes (fixed summation order, no
+ * atomics), so equal weights give bit-identical y.  Enqueued on `stream`;
+ * returns without waiting.  DF11_E_UNSUPPORTED for shapes outside the
+ * requirements above, DF11_E_BUFFER_TOO_SMALL for a short workspace. */
+int df11_block_gemm(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats,
+                    uint32_t n_mats, const uint16_t *const *x, uint32_t tokens, float *const *y,
+                    void *workspace, uint64_t workspace_bytes, hipStream_t stream);
+
+/* df11_decode_block(dev, weights_out, stream) followed by
+ * df11_block_gemm(weights_out, dev->sizes.n_elems, ...) on the same stream:
+ * one transformer block decompressed into the caller's BF16 workspace
+ * (weights_out, 2*n_elems bytes) and consumed by its matrix products. */
+int df11_block_forward(const df11_stream *dev, uint16_t *weights_out, const df11_matrix *mats,
+                       uint32_t n_mats, const uint16_t *const *x, uint32_t tokens,
+                       float *const *y, void *workspace, uint64_t workspace_bytes,
+                       hipStream_t stream);
 
 /* Static description of a status code. */
 const char *df11_strerror(int status);

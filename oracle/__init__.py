@@ -216,3 +216,22 @@ def compress(w, max_len: int = 32, n_bytes: int = 8, threads: int = 256) -> dict
     return dict(counts=counts, lengths=lengths, codes=codes, total_bits=total_bits, exp=exp,
                 sm=sm, gaps=gaps, gaps_packed=packed, block_pos=bp, n=w.size, n_bytes=n_bytes,
                 threads=threads, **lay)
+
+
+# ------------------------------------------------------------ matrix products
+def bf16_to_f64(bits) -> np.ndarray:
+    """BF16 bit patterns -> float64: a BF16 value is the float32 whose upper 16
+    bits are the pattern and whose lower 16 bits are zero."""
+    b = np.ascontiguousarray(bits)
+    if b.dtype != np.uint16:
+        b = b.view(np.uint16)
+    return (b.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+
+
+def linear(x_bits, w_bits) -> np.ndarray:
+    """Y = X W^T in float64 for BF16 X (tokens x k) and W (rows x k): the
+    product the decompressed weights feed (Sec. 2.3.3), with every BF16 product
+    exact and the sums rounded only at float64 precision."""
+    x = bf16_to_f64(x_bits)
+    w = bf16_to_f64(w_bits)
+    return x @ w.T

@@ -26,8 +26,11 @@ ERRORS = {
 EXPORTS = (
     "df11_build_codebook", "df11_codebook_from_counts", "df11_encoded_sizes", "df11_encode",
     "df11_build_tables", "df11_validate", "df11_decode_block", "df11_decode_launch_shape",
-    "df11_strerror",
+    "df11_gemm_workspace_bytes", "df11_block_gemm", "df11_block_forward", "df11_strerror",
 )
+
+MAX_MATRICES = 8  # DF11_MAX_MATRICES
+MAX_TOKENS = 64   # DF11_MAX_TOKENS
 
 
 class Codebook(ctypes.Structure):
@@ -71,6 +74,10 @@ class Stream(ctypes.Structure):
                 ("layout", Layout)]
 
 
+class Matrix(ctypes.Structure):
+    _fields_ = [("offset", ctypes.c_uint64), ("rows", ctypes.c_uint32), ("cols", ctypes.c_uint32)]
+
+
 DEFAULT_LAYOUT = (8, 64, 11)  # bytes per thread, threads per block, table index bits
 
 _lib = None
@@ -105,6 +112,11 @@ def lib():
         "df11_decode_block": [P(Stream), vp, vp],
         "df11_decode_launch_shape": [P(Stream), P(ctypes.c_uint32), P(ctypes.c_uint32),
                                      P(ctypes.c_uint32)],
+        "df11_gemm_workspace_bytes": [P(Matrix), ctypes.c_uint32, ctypes.c_uint32, P(u64)],
+        "df11_block_gemm": [vp, u64, P(Matrix), ctypes.c_uint32, P(vp), ctypes.c_uint32, P(vp),
+                            vp, u64, vp],
+        "df11_block_forward": [P(Stream), vp, P(Matrix), ctypes.c_uint32, P(vp), ctypes.c_uint32,
+                               P(vp), vp, u64, vp],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -283,3 +295,68 @@ def decode_block(ds: DeviceStream, out=None, stream=None):
     _check(lib().df11_decode_block(ctypes.byref(ds.struct()), ctypes.c_void_p(out.data_ptr()),
                                    ctypes.c_void_p(handle)), "df11_decode_block")
     return out
+
+
+# ------------------------------------------------------- decode-then-GEMM driver
+def _mats(mats) -> "ctypes.Array":
+    arr = (Matrix * len(mats))()
+    for i, (off, rows, cols) in enumerate(mats):
+        arr[i] = Matrix(int(off), int(rows), int(cols))
+    return arr
+
+
+def gemm_workspace_bytes(mats, tokens: int) -> int:
+    """Workspace bytes block_gemm / block_forward need (mats: (offset, rows, cols))."""
+    m = _mats(mats)
+    out = ctypes.c_uint64()
+    _check(lib().df11_gemm_workspace_bytes(m, len(mats), int(tokens), ctypes.byref(out)),
+           "df11_gemm_workspace_bytes")
+    return int(out.value)
+
+
+def _gemm_marshal(mats, xs, ys, workspace):
+    if not (len(mats) == len(xs) == len(ys)):
+        raise ValueError("one activation and one output tensor per matrix")
+    tokens = int(xs[0].shape[0])
+    for (off, rows, cols), x, y in zip(mats, xs, ys):
+        if tuple(x.shape) != (tokens, cols) or x.element_size() != 2 or not x.is_contiguous():
+            raise ValueError("x[m] must be a contiguous bf16 tensor of shape (tokens, cols)")
+        if tuple(y.shape) != (tokens, rows) or y.element_size() != 4 or not y.is_contiguous():
+            raise ValueError("y[m] must be a contiguous fp32 tensor of shape (tokens, rows)")
+    xp = (ctypes.c_void_p * len(xs))(*[x.data_ptr() for x in xs])
+    yp = (ctypes.c_void_p * len(ys))(*[y.data_ptr() for y in ys])
+    ws_ptr = workspace.data_ptr() if workspace is not None else 0
+    ws_bytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    return _mats(mats), xp, yp, tokens, ws_ptr, ws_bytes
+
+
+def _handle(stream, device):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def block_gemm(weights, mats, xs, ys, workspace=None, stream=None):
+    """ys[m] = xs[m] @ W_m^T for the matrices (offset, rows, cols) of the BF16
+    block ``weights`` (device tensor), fp32 results written into ys."""
+    m, xp, yp, tokens, ws_ptr, ws_bytes = _gemm_marshal(mats, xs, ys, workspace)
+    _check(lib().df11_block_gemm(ctypes.c_void_p(weights.data_ptr()), weights.numel(), m,
+                                 len(mats), xp, tokens, yp, ctypes.c_void_p(ws_ptr), ws_bytes,
+                                 ctypes.c_void_p(_handle(stream, weights.device))),
+           "df11_block_gemm")
+    return ys
+
+
+def block_forward(ds: DeviceStream, weights_out, mats, xs, ys, workspace=None, stream=None):
+    """Decode ``ds`` into ``weights_out`` (bf16 device tensor of n_elems), then
+    block_gemm on it, all on one stream."""
+    if weights_out.numel() < ds.n_elems or weights_out.element_size() != 2:
+        raise ValueError("weights_out must be a 2-byte tensor with n_elems elements")
+    m, xp, yp, tokens, ws_ptr, ws_bytes = _gemm_marshal(mats, xs, ys, workspace)
+    _check(lib().df11_block_forward(ctypes.byref(ds.struct()),
+                                    ctypes.c_void_p(weights_out.data_ptr()), m, len(mats), xp,
+                                    tokens, yp, ctypes.c_void_p(ws_ptr), ws_bytes,
+                                    ctypes.c_void_p(_handle(stream, ds.device))),
+           "df11_block_forward")
+    return ys

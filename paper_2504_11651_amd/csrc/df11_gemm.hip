@@ -1,0 +1,355 @@
+// Matrix products of a decompressed transformer block on the gfx950 matrix
+// cores: y[m] = x[m] * W_m^T for the block's matrices, BF16 inputs, fp32
+// accumulation (the consumer of the decoded weights in Sec. 2.3.3; the
+// batch-size experiments of Sec. 3 time decompression plus these products).
+//
+// With at most 64 activation rows the products are bound by streaming the
+// weights from HBM, so the design reads every weight once, with 16-byte
+// loads, and keeps several kilobytes in flight per wave:
+//   - one wavefront computes a tile of 16 output features x all tokens over a
+//     contiguous range of k; all matrices of the block share one launch;
+//   - per 64 k a lane loads 2 x 8 BF16 of one weight row (lanes 16g..16g+15
+//     take rows 0..15 at k offset 16g) and the matching activations, and
+//     issues v_mfma_f32_16x16x32_bf16 twice per 16-token slice; A (tokens)
+//     and B (features) use the same assignment of k to lanes, so the dot
+//     products cover each k once whatever order the unit sums in;
+//   - a matrix wider than 4096 columns is split into k ranges; each range
+//     writes fp32 partial sums, and a second kernel adds them in a fixed
+//     order, so results are deterministic (no atomics).
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "df11.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr uint32_t kTileRows = 16;   // output features per wave
+constexpr uint32_t kKStep = 64;      // k per inner step: two MFMAs
+constexpr uint32_t kUnroll = 4;      // inner steps whose weight loads are issued together
+constexpr uint32_t kKPerIter = kKStep * kUnroll;
+constexpr uint32_t kKTarget = 4096;  // k range of one wave before a matrix is split
+constexpr uint32_t kWaves = 4;       // waves per workgroup
+constexpr uint32_t kMax = DF11_MAX_MATRICES;
+
+struct GemmArgs {
+    const uint16_t *w;
+    float *part;
+    uint32_t n_mats;
+    uint32_t tokens;
+    uint32_t num_tiles;
+    uint32_t tile_start[kMax + 1];  // prefix sums of tiles per matrix
+    uint32_t ksplit[kMax];          // k ranges per matrix
+    uint32_t kchunk[kMax];          // k per range (multiple of kKPerIter)
+    uint32_t rows[kMax];
+    uint32_t cols[kMax];
+    uint64_t w_off[kMax];           // weights
+    uint64_t part_off[kMax];        // floats (split matrices only)
+    const uint16_t *x[kMax];
+    float *y[kMax];
+};
+
+struct ReduceArgs {
+    const float *part;
+    uint32_t n_mats;
+    uint32_t tokens;
+    uint32_t total;                 // outputs of all split matrices
+    uint32_t out_start[kMax + 1];   // prefix sums of tokens*rows over split matrices
+    uint32_t ksplit[kMax];
+    uint32_t rows[kMax];
+    uint64_t part_off[kMax];
+    float *y[kMax];
+};
+
+__device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b ? a : b; }
+
+__device__ __forceinline__ uint4 load16(const uint16_t *p) {
+    return *reinterpret_cast<const uint4 *>(p);
+}
+
+__device__ __forceinline__ uint4 masked(uint4 v, uint32_t m) {
+    return make_uint4(v.x & m, v.y & m, v.z & m, v.w & m);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// MT = 16-token slices (tokens <= 16 * MT).
+template <uint32_t MT>
+__global__ __launch_bounds__(64 * kWaves) void gemm_tiles_kernel(GemmArgs a) {
+    const uint32_t lane = threadIdx.x & 63u;
+    const uint32_t tile =
+        blockIdx.x * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    if (tile >= a.num_tiles) return;
+
+    // matrix of this tile (uniform; constant-index selects keep the kernel
+    // arguments in scalar registers)
+    uint32_t start = 0, ksplit = 1, kchunk = 0, rows = 0, cols = 0;
+    uint64_t w_off = 0, part_off = 0;
+    const uint16_t *x = nullptr;
+    float *y = nullptr;
+#pragma unroll
+    for (uint32_t i = 0; i < kMax; ++i) {
+        if (i < a.n_mats && tile >= a.tile_start[i]) {
+            start = a.tile_start[i];
+            ksplit = a.ksplit[i];
+            kchunk = a.kchunk[i];
+            rows = a.rows[i];
+            cols = a.cols[i];
+            w_off = a.w_off[i];
+            part_off = a.part_off[i];
+            x = a.x[i];
+            y = a.y[i];
+        }
+    }
+    const uint32_t local = tile - start;
+    const uint32_t rb = local / ksplit;
+    const uint32_t s = local - rb * ksplit;
+    const uint32_t k0 = s * kchunk;
+    const uint32_t k1 = umin(cols, k0 + kchunk);
+
+    const uint32_t j = lane & 15u;   // feature row (B) / token row (A) in the slice
+    const uint32_t g = lane >> 4;    // k group
+    const uint16_t *wrow = a.w + w_off + static_cast<uint64_t>(rb * kTileRows + j) * cols + 16u * g;
+    // rows of x past the last token read token 0 and are masked to zero
+    const uint16_t *xrow[MT];
+    uint32_t xmask[MT];
+#pragma unroll
+    for (uint32_t mt = 0; mt < MT; ++mt) {
+        const uint32_t t = mt * 16u + j;
+        xmask[mt] = t < a.tokens ? ~0u : 0u;
+        xrow[mt] = x + static_cast<uint64_t>(t < a.tokens ? t : 0u) * cols + 16u * g;
+    }
+
+    f32x4 acc[MT];
+#pragma unroll
+    for (uint32_t mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    // one 64-k step: activations of every slice against the loaded weights
+    auto step = [&](uint32_t kk, uint4 w0, uint4 w1) {
+#pragma unroll
+        for (uint32_t mt = 0; mt < MT; ++mt) {
+            const uint4 x0 = masked(load16(xrow[mt] + kk), xmask[mt]);
+            const uint4 x1 = masked(load16(xrow[mt] + kk + 8u), xmask[mt]);
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x0), as_bf16x8(w0), acc[mt],
+                                                              0, 0, 0);
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x1), as_bf16x8(w1), acc[mt],
+                                                              0, 0, 0);
+        }
+    };
+    uint32_t k = k0;
+    for (; k + kKPerIter <= k1; k += kKPerIter) {
+        // the weight loads of kUnroll steps are issued before their products
+        uint4 W[kUnroll][2];
+#pragma unroll
+        for (uint32_t u = 0; u < kUnroll; ++u) {
+            W[u][0] = load16(wrow + k + u * kKStep);
+            W[u][1] = load16(wrow + k + u * kKStep + 8u);
+        }
+#pragma unroll
+        for (uint32_t u = 0; u < kUnroll; ++u) step(k + u * kKStep, W[u][0], W[u][1]);
+    }
+    for (; k < k1; k += kKStep) step(k, load16(wrow + k), load16(wrow + k + 8u));
+
+    // acc[mt][r] = sum over the range for token 16*mt + 4*g + r, feature
+    // rb*16 + j
+    const uint32_t feature = rb * kTileRows + j;
+#pragma unroll
+    for (uint32_t mt = 0; mt < MT; ++mt) {
+#pragma unroll
+        for (uint32_t r = 0; r < 4; ++r) {
+            const uint32_t t = mt * 16u + 4u * g + r;
+            if (t >= a.tokens) continue;
+            if (ksplit == 1) {
+                y[static_cast<uint64_t>(t) * rows + feature] = acc[mt][r];
+            } else {
+                const uint64_t idx = part_off +
+                    (static_cast<uint64_t>(rb * ksplit + s) * a.tokens + t) * kTileRows + j;
+                a.part[idx] = acc[mt][r];
+            }
+        }
+    }
+}
+
+// y[t][f] = sum over k ranges s = 0, 1, ... of the partial sums, in that order.
+__global__ __launch_bounds__(256) void gemm_reduce_kernel(ReduceArgs a) {
+    const uint32_t i = blockIdx.x * 256u + threadIdx.x;
+    if (i >= a.total) return;
+    uint32_t m = 0;
+#pragma unroll
+    for (uint32_t q = 1; q < kMax; ++q)
+        if (q < a.n_mats && i >= a.out_start[q]) m = q;
+    uint32_t start = 0, ksplit = 1, rows = 1;
+    uint64_t part_off = 0;
+    float *y = nullptr;
+#pragma unroll
+    for (uint32_t q = 0; q < kMax; ++q) {
+        if (q == m) {
+            start = a.out_start[q];
+            ksplit = a.ksplit[q];
+            rows = a.rows[q];
+            part_off = a.part_off[q];
+            y = a.y[q];
+        }
+    }
+    const uint32_t local = i - start;
+    const uint32_t t = local / rows;
+    const uint32_t f = local - t * rows;
+    const uint32_t rb = f / kTileRows;
+    const uint32_t j = f - rb * kTileRows;
+    float sum = 0.f;
+    for (uint32_t s = 0; s < ksplit; ++s)
+        sum += a.part[part_off + (static_cast<uint64_t>(rb * ksplit + s) * a.tokens + t) * kTileRows + j];
+    y[static_cast<uint64_t>(t) * rows + f] = sum;
+}
+
+// Work split of one matrix: k ranges of at most about kKTarget, each a
+// multiple of kKPerIter except the last.
+void split_of(uint32_t cols, uint32_t *ksplit, uint32_t *kchunk) {
+    uint32_t ks = (cols + kKTarget - 1) / kKTarget;
+    if (ks == 0) ks = 1;
+    uint32_t kc = (cols + ks - 1) / ks;
+    kc = (kc + kKPerIter - 1) / kKPerIter * kKPerIter;
+    ks = (cols + kc - 1) / kc;  // no empty range
+    *ksplit = ks;
+    *kchunk = kc;
+}
+
+int check_mats(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens) {
+    if (!mats || n_mats == 0 || n_mats > kMax) return DF11_E_INVALID_ARG;
+    if (tokens == 0 || tokens > DF11_MAX_TOKENS) return DF11_E_UNSUPPORTED;
+    for (uint32_t m = 0; m < n_mats; ++m) {
+        const df11_matrix &d = mats[m];
+        if (d.rows == 0 || d.cols == 0) return DF11_E_INVALID_ARG;
+        if (d.rows % kTileRows || d.cols % kKStep || d.offset % 8) return DF11_E_UNSUPPORTED;
+    }
+    return DF11_OK;
+}
+
+uint64_t workspace_floats(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens) {
+    uint64_t f = 0;
+    for (uint32_t m = 0; m < n_mats; ++m) {
+        uint32_t ks, kc;
+        split_of(mats[m].cols, &ks, &kc);
+        if (ks > 1) f += static_cast<uint64_t>(mats[m].rows) * ks * tokens;
+    }
+    return f;
+}
+
+// Checks every argument and fills the kernel arguments; enqueues nothing.
+int plan(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats, uint32_t n_mats,
+         const uint16_t *const *x, uint32_t tokens, float *const *y, void *workspace,
+         uint64_t workspace_bytes, GemmArgs *gp, ReduceArgs *rp) {
+    int rc = check_mats(mats, n_mats, tokens);
+    if (rc) return rc;
+    if (!weights || !x || !y || (reinterpret_cast<uintptr_t>(weights) & 15u))
+        return DF11_E_INVALID_ARG;
+    const uint64_t need = 4 * workspace_floats(mats, n_mats, tokens);
+    if (need > workspace_bytes) return DF11_E_BUFFER_TOO_SMALL;
+    if (need && (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 15u)))
+        return DF11_E_INVALID_ARG;
+
+    GemmArgs g{};
+    ReduceArgs r{};
+    g.w = weights;
+    g.part = static_cast<float *>(workspace);
+    r.part = static_cast<const float *>(workspace);
+    g.n_mats = r.n_mats = n_mats;
+    g.tokens = r.tokens = tokens;
+    uint64_t tiles = 0, part = 0, outs = 0;
+    for (uint32_t m = 0; m < n_mats; ++m) {
+        const df11_matrix &d = mats[m];
+        if (d.offset > n_weights || static_cast<uint64_t>(d.rows) * d.cols > n_weights - d.offset)
+            return DF11_E_INVALID_ARG;
+        if (!x[m] || !y[m] || (reinterpret_cast<uintptr_t>(x[m]) & 15u) ||
+            (reinterpret_cast<uintptr_t>(y[m]) & 3u))
+            return DF11_E_INVALID_ARG;
+        uint32_t ks, kc;
+        split_of(d.cols, &ks, &kc);
+        g.tile_start[m] = static_cast<uint32_t>(tiles);
+        g.ksplit[m] = r.ksplit[m] = ks;
+        g.kchunk[m] = kc;
+        g.rows[m] = r.rows[m] = d.rows;
+        g.cols[m] = d.cols;
+        g.w_off[m] = d.offset;
+        g.part_off[m] = r.part_off[m] = part;
+        g.x[m] = x[m];
+        g.y[m] = r.y[m] = y[m];
+        r.out_start[m] = static_cast<uint32_t>(outs);
+        tiles += static_cast<uint64_t>(d.rows / kTileRows) * ks;
+        if (ks > 1) {
+            part += static_cast<uint64_t>(d.rows) * ks * tokens;
+            outs += static_cast<uint64_t>(d.rows) * tokens;
+        }
+        if (tiles > 0xFFFFFFFFull || outs > 0xFFFFFFFFull) return DF11_E_UNSUPPORTED;
+    }
+    for (uint32_t m = n_mats; m <= kMax; ++m) {
+        g.tile_start[m] = static_cast<uint32_t>(tiles);
+        r.out_start[m] = static_cast<uint32_t>(outs);
+    }
+    g.num_tiles = static_cast<uint32_t>(tiles);
+    r.total = static_cast<uint32_t>(outs);
+    *gp = g;
+    *rp = r;
+    return DF11_OK;
+}
+
+int launch(const GemmArgs &g, const ReduceArgs &r, hipStream_t stream) {
+    const uint32_t mt = (g.tokens + 15) / 16;
+    const dim3 grid((g.num_tiles + kWaves - 1) / kWaves), block(64 * kWaves);
+    switch (mt) {
+    case 1: hipLaunchKernelGGL(gemm_tiles_kernel<1>, grid, block, 0, stream, g); break;
+    case 2: hipLaunchKernelGGL(gemm_tiles_kernel<2>, grid, block, 0, stream, g); break;
+    case 3: hipLaunchKernelGGL(gemm_tiles_kernel<3>, grid, block, 0, stream, g); break;
+    default: hipLaunchKernelGGL(gemm_tiles_kernel<4>, grid, block, 0, stream, g); break;
+    }
+    if (hipGetLastError() != hipSuccess) return DF11_E_HIP;
+    if (r.total) {
+        hipLaunchKernelGGL(gemm_reduce_kernel, dim3((r.total + 255) / 256), dim3(256), 0, stream, r);
+        if (hipGetLastError() != hipSuccess) return DF11_E_HIP;
+    }
+    return DF11_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int df11_gemm_workspace_bytes(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens,
+                              uint64_t *bytes) {
+    int rc = check_mats(mats, n_mats, tokens);
+    if (rc) return rc;
+    if (!bytes) return DF11_E_INVALID_ARG;
+    *bytes = 4 * workspace_floats(mats, n_mats, tokens);
+    return DF11_OK;
+}
+
+int df11_block_gemm(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats,
+                    uint32_t n_mats, const uint16_t *const *x, uint32_t tokens, float *const *y,
+                    void *workspace, uint64_t workspace_bytes, hipStream_t stream) {
+    GemmArgs g;
+    ReduceArgs r;
+    int rc = plan(weights, n_weights, mats, n_mats, x, tokens, y, workspace, workspace_bytes, &g, &r);
+    if (rc) return rc;
+    return launch(g, r, stream);
+}
+
+int df11_block_forward(const df11_stream *dev, uint16_t *weights_out, const df11_matrix *mats,
+                       uint32_t n_mats, const uint16_t *const *x, uint32_t tokens,
+                       float *const *y, void *workspace, uint64_t workspace_bytes,
+                       hipStream_t stream) {
+    if (!dev) return DF11_E_INVALID_ARG;
+    // every argument is checked before anything is enqueued
+    GemmArgs g;
+    ReduceArgs r;
+    int rc = plan(weights_out, dev->sizes.n_elems, mats, n_mats, x, tokens, y, workspace,
+                  workspace_bytes, &g, &r);
+    if (rc) return rc;
+    rc = df11_decode_block(dev, weights_out, stream);
+    if (rc) return rc;
+    return launch(g, r, stream);
+}
+
+}  // extern "C"

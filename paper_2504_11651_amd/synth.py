@@ -125,6 +125,14 @@ def llama3_8b_stack_block(i: int):
     return _block(LLAMA3_8B_BLOCK, 5, i, 0.008, 0.04)
 
 
+def activations(tokens: int, cols: int, *key: int) -> np.ndarray:
+    """tokens x cols BF16 activations ~ N(0, 1), row-major (uint16 bit patterns),
+    from the generator seeded by ``key``."""
+    out = np.empty(tokens * cols, np.uint16)
+    _fill_pieces(out, (200, *key), _normal(1.0))
+    return out.reshape(tokens, cols)
+
+
 def heavy_tailed_block(n: int = 218_103_808, seed: int = 0) -> np.ndarray:
     """Stress block: 0.02 * Student-t(3), then 0.01% outliers of magnitude
     2**U(0, 6) with random sign and 1% exact +0.0, at disjoint uniformly drawn

@@ -1,0 +1,96 @@
+"""Host-side checks of the decode-then-GEMM driver's C ABI: workspace sizing
+and argument validation.  Every call here is rejected before anything is
+enqueued, so no device is touched (the pointers are never dereferenced)."""
+import ctypes
+
+import pytest
+
+from paper_2504_11651_amd import codec, synth
+
+from conftest import gpu_available
+
+# argument checks only; with a device present the GPU tests cover these paths
+pytestmark = pytest.mark.skipif(gpu_available(), reason="host-only argument checks")
+
+def llama_mats():
+    mats, off = [], 0
+    for _, r, c in synth.LLAMA3_8B_BLOCK:
+        mats.append((off, r, c))
+        off += r * c
+    return mats, off
+
+
+def test_workspace_closed_form():
+    # only down (14336 columns) is split: 4 k-ranges of 3584; partial sums of
+    # 4096 rows x 4 ranges x tokens floats
+    mats, _ = llama_mats()
+    for t in (1, 7, 16, 64):
+        assert codec.gemm_workspace_bytes(mats, t) == 4 * 4096 * 4 * t
+    assert codec.gemm_workspace_bytes([(0, 16, 4096)], 5) == 0
+    # 8192 columns -> 2 ranges; 28672 -> 7 ranges
+    assert codec.gemm_workspace_bytes([(0, 32, 8192)], 3) == 4 * 32 * 2 * 3
+    assert codec.gemm_workspace_bytes([(0, 32, 28672)], 2) == 4 * 32 * 7 * 2
+
+
+@pytest.mark.parametrize("mats,tokens,rc", [
+    ([(0, 16, 64)], 0, -6),        # no tokens
+    ([(0, 16, 64)], 65, -6),       # more than 64 tokens
+    ([(0, 15, 64)], 1, -6),        # rows not a multiple of 16
+    ([(0, 16, 96)], 1, -6),        # cols not a multiple of 64
+    ([(4, 16, 64)], 1, -6),        # offset not 16-byte aligned
+    ([(0, 0, 64)], 1, -1),         # empty matrix
+    ([], 1, -1),                   # no matrices
+    ([(0, 16, 64)] * 9, 1, -1),    # more than 8 matrices
+])
+def test_shape_rejections(mats, tokens, rc):
+    L = codec.lib()
+    m = codec._mats(mats) if mats else None
+    out = ctypes.c_uint64()
+    assert L.df11_gemm_workspace_bytes(m, len(mats), tokens, ctypes.byref(out)) == rc
+
+
+def _call_gemm(weights, n_weights, mats, xs, ys, tokens, ws, ws_bytes):
+    L = codec.lib()
+    m = codec._mats(mats)
+    xp = (ctypes.c_void_p * len(xs))(*xs)
+    yp = (ctypes.c_void_p * len(ys))(*ys)
+    return L.df11_block_gemm(ctypes.c_void_p(weights), n_weights, m, len(mats), xp, tokens, yp,
+                             ctypes.c_void_p(ws), ws_bytes, ctypes.c_void_p(0))
+
+
+A = 1 << 20  # a 16-byte aligned stand-in address (never dereferenced)
+
+
+def test_argument_rejections():
+    mats = [(0, 16, 64)]
+    assert _call_gemm(0, 1024, mats, [A], [A], 1, 0, 0) == -1           # null weights
+    assert _call_gemm(A + 2, 1024, mats, [A], [A], 1, 0, 0) == -1       # misaligned weights
+    assert _call_gemm(A, 1023, mats, [A], [A], 1, 0, 0) == -1           # matrix past the block
+    assert _call_gemm(A, 1024, mats, [A + 8], [A], 1, 0, 0) == -1       # misaligned x
+    assert _call_gemm(A, 1024, mats, [A], [A + 2], 1, 0, 0) == -1       # misaligned y
+    assert _call_gemm(A, 1024, mats, [0], [A], 1, 0, 0) == -1           # null x
+    # a split matrix needs a workspace
+    big = [(0, 16, 8192)]
+    need = codec.gemm_workspace_bytes(big, 2)
+    assert _call_gemm(A, 16 * 8192, big, [A], [A], 2, A, need - 4) == -3
+    assert _call_gemm(A, 16 * 8192, big, [A], [A], 2, 0, need) == -1    # null workspace
+    assert _call_gemm(A, 16 * 8192, big, [A], [A], 2, A + 4, need) == -1
+
+
+def test_block_forward_checks_gemm_arguments_before_decoding():
+    # an invalid matrix list is rejected before the decode is enqueued
+    L = codec.lib()
+    st = codec.Stream()
+    st.sizes.n_elems = 1024
+    st.layout.bytes_per_thread, st.layout.threads_per_block, st.layout.lut_bits = 8, 64, 11
+    m = codec._mats([(0, 16, 64)])
+    xp = (ctypes.c_void_p * 1)(A)
+    yp = (ctypes.c_void_p * 1)(A)
+    rc = L.df11_block_forward(ctypes.byref(st), ctypes.c_void_p(A), m, 1, xp, 65, yp,
+                              ctypes.c_void_p(0), 0, ctypes.c_void_p(0))
+    assert rc == -6
+    rc = L.df11_block_forward(ctypes.byref(st), ctypes.c_void_p(A + 2), m, 1, xp, 1, yp,
+                              ctypes.c_void_p(0), 0, ctypes.c_void_p(0))
+    assert rc == -1
+    assert L.df11_block_forward(None, ctypes.c_void_p(A), m, 1, xp, 1, yp, ctypes.c_void_p(0), 0,
+                                ctypes.c_void_p(0)) == -1

@@ -383,3 +383,82 @@ def test_gaussian_statistics_resemble_the_paper():
     assert 15 <= int((counts > 0).sum()) <= 45
     bits_per_weight = 8 + cost(counts, lengths) / counts.sum()
     assert 10.4 < bits_per_weight < 11.2
+
+
+# ------------------------------------------------ matrix products (linear)
+def test_bf16_to_f64_ieee_values():
+    # BF16 = upper half of an IEEE binary32: values fixed by that format
+    bits = np.array([0x3F80, 0xBF80, 0x4000, 0x3F00, 0x4049, 0x0000, 0x8000, 0x0001, 0x7F7F,
+                     0x7F80, 0xFF80], np.uint16)
+    want = [1.0, -1.0, 2.0, 0.5, 3.140625, 0.0, -0.0, 2.0 ** -133, (2 - 2 ** -7) * 2.0 ** 127,
+            math.inf, -math.inf]
+    got = oracle.bf16_to_f64(bits)
+    for g, w in zip(got, want):
+        assert g == w and math.copysign(1, g) == math.copysign(1, w)
+    assert math.isnan(oracle.bf16_to_f64(np.array([0x7FC0], np.uint16))[0])
+
+
+def _bits_of_small_ints(vals) -> np.ndarray:
+    # small integers are exact in BF16 (8-bit significand): build their bits
+    # from sign, exponent and mantissa by hand
+    out = []
+    for v in vals:
+        v = int(v)
+        if v == 0:
+            out.append(0)
+            continue
+        s, a = (1, -v) if v < 0 else (0, v)
+        e = a.bit_length() - 1
+        mant = (a << (7 - e)) & 0x7F if e <= 7 else None
+        assert mant is not None and (a >> e) == 1 and a == ((0x80 | mant) << e) >> 7
+        out.append((s << 15) | ((e + 127) << 7) | mant)
+    return np.array(out, np.uint16)
+
+
+def test_linear_brute_force_exact_rationals():
+    # tiny non-square shapes with distinct small-integer entries: the exact
+    # result is known, and a transposed operand or swapped index changes it
+    from fractions import Fraction
+    rng = np.random.default_rng(3)
+    for t, rows, k in [(1, 3, 2), (2, 3, 5), (3, 2, 7), (4, 5, 3)]:
+        xi = rng.integers(-9, 10, size=(t, k))
+        wi = rng.integers(-9, 10, size=(rows, k))
+        y = oracle.linear(_bits_of_small_ints(xi.ravel()).reshape(t, k),
+                          _bits_of_small_ints(wi.ravel()).reshape(rows, k))
+        assert y.shape == (t, rows)
+        for a in range(t):
+            for r in range(rows):
+                exact = sum(Fraction(int(xi[a, q])) * Fraction(int(wi[r, q])) for q in range(k))
+                assert y[a, r] == float(exact)
+
+
+def test_linear_identity_and_selection():
+    # x = identity rows select rows of W: y[t][r] = W[r][t]
+    k, rows = 6, 4
+    eye = _bits_of_small_ints(np.eye(k, dtype=int).ravel()).reshape(k, k)
+    wi = np.arange(rows * k).reshape(rows, k) - 11
+    y = oracle.linear(eye, _bits_of_small_ints(wi.ravel()).reshape(rows, k))
+    assert np.array_equal(y, wi.T.astype(np.float64))
+
+
+def test_linear_error_bound_on_random_bf16():
+    # float64 sums of exact BF16 products: within k * 2^-53 * sum|x w| of the
+    # exact value, checked against exact integer arithmetic on scaled values
+    x = synth.activations(3, 257, 9, 9)
+    w = synth.gaussian(5 * 257, 0.02, 11).reshape(5, 257)
+    y = oracle.linear(x, w)
+
+    def as_int(bits):  # value * 2^150 is an integer for every finite BF16
+        b = bits.astype(np.int64)
+        sign = np.where(b >> 15, -1, 1)
+        e, m = (b >> 7) & 0xFF, b & 0x7F
+        sig = np.where(e == 0, m, m | 0x80)
+        sh = np.where(e == 0, 1, e) - 1 - 7 + 150 - 127 + 1
+        return [int(sg) * (int(sv) << int(s)) for sg, sv, s in zip(sign, sig, sh)]
+    xs = [as_int(r) for r in x]
+    ws = [as_int(r) for r in w]
+    for a in range(3):
+        for r in range(5):
+            exact = sum(p * q for p, q in zip(xs[a], ws[r])) / 2.0 ** 300
+            mag = sum(abs(p * q) for p, q in zip(xs[a], ws[r])) / 2.0 ** 300
+            assert abs(y[a, r] - exact) <= 257 * 2.0 ** -53 * mag + 1e-300
