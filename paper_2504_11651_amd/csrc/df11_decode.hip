@@ -171,7 +171,7 @@ __device__ __forceinline__ ChunkWords load_chunk(const DecodeArgs &a, uint32_t b
 
 // Lookups kept in registers between the count phase and the write phase;
 // a chunk needing more (short codes, 4 per lookup) continues in a loop.
-constexpr int kKeep = 12;
+constexpr int kKeep = 10;
 // 8-element output groups whose sign/mantissa bytes are fetched at block start.
 constexpr int kPre = 4;
 
@@ -420,11 +420,17 @@ __global__ __launch_bounds__(64 * W) void df11_decode_wave_kernel(DecodeArgs a) 
         uint32_t sy[kKeep], npk[(kKeep + 3) / 4], p_rest;
         const uint32_t cnt = decode_count(tb, ch, sy, npk, &p_rest);
         const uint32_t excl = wave_inclusive_scan(cnt) - cnt;
+        // Waves near their memory phase issue first: the CU's decoding waves
+        // (priority 0) fill the gaps, and the loads and stores of the waves
+        // that have finished decoding reach the memory system sooner.
+        __builtin_amdgcn_s_setprio(1);
         wave_lds_sync();
         emit_exponents(tb, ch, sy, npk, p_rest, r.shift + excl, buf32, cap);
         wave_lds_sync();
 
+        __builtin_amdgcn_s_setprio(2);
         assemble_block(a, r, buf, lane, 64u, S);
+        __builtin_amdgcn_s_setprio(0);
         cw = nxt;
         ch = chunk_setup(a, cw, bn * 64u + lane);
         r = block_range(a, cw);
