@@ -41,7 +41,9 @@ struct GemmArgs {
     uint32_t n_mats;
     uint32_t tokens;
     uint32_t num_tiles;
-    uint32_t tile_start[kMax + 1];  // prefix sums of tiles per matrix
+    uint32_t num_wg;
+    uint32_t tile_start[kMax + 1];  // prefix sums of 16-feature tiles per matrix
+    uint32_t wg_start[kMax + 1];    // prefix sums of 64-feature workgroup tiles
     uint32_t ksplit[kMax];          // k ranges per matrix
     uint32_t kchunk[kMax];          // k per range (multiple of kKPerIter)
     uint32_t rows[kMax];
@@ -76,68 +78,91 @@ __device__ __forceinline__ uint4 masked(uint4 v, uint32_t m) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
-// MT = 16-token slices (tokens <= 16 * MT).
+struct Mat {
+    uint32_t ksplit, kchunk, rows, cols;
+    uint64_t w_off, part_off;
+    const uint16_t *x;
+    float *y;
+};
+
+// Matrix whose work items [start[i], start[i+1]) contain idx (uniform;
+// constant-index selects keep the kernel arguments in scalar registers).
+__device__ __forceinline__ Mat select_matrix(const GemmArgs &a, const uint32_t (&start)[kMax + 1],
+                                             uint32_t idx, uint32_t *first) {
+    Mat m{1, 0, 0, 0, 0, 0, nullptr, nullptr};
+    *first = 0;
+#pragma unroll
+    for (uint32_t i = 0; i < kMax; ++i) {
+        if (i < a.n_mats && idx >= start[i]) {
+            *first = start[i];
+            m.ksplit = a.ksplit[i];
+            m.kchunk = a.kchunk[i];
+            m.rows = a.rows[i];
+            m.cols = a.cols[i];
+            m.w_off = a.w_off[i];
+            m.part_off = a.part_off[i];
+            m.x = a.x[i];
+            m.y = a.y[i];
+        }
+    }
+    return m;
+}
+
+// acc[mt][r] holds the sum over k range s for token 16*mt + 4*g + r and
+// feature 16*rb + j: written to y, or to the partial sums of a split matrix.
 template <uint32_t MT>
+__device__ __forceinline__ void write_tile(const GemmArgs &a, const Mat &m, uint32_t rb, uint32_t s,
+                                           uint32_t j, uint32_t g, const f32x4 (&acc)[MT]) {
+    const uint32_t feature = rb * kTileRows + j;
+#pragma unroll
+    for (uint32_t mt = 0; mt < MT; ++mt) {
+#pragma unroll
+        for (uint32_t r = 0; r < 4; ++r) {
+            const uint32_t t = mt * 16u + 4u * g + r;
+            if (t >= a.tokens) continue;
+            if (m.ksplit == 1) {
+                m.y[static_cast<uint64_t>(t) * m.rows + feature] = acc[mt][r];
+            } else {
+                const uint64_t idx = m.part_off +
+                    (static_cast<uint64_t>(rb * m.ksplit + s) * a.tokens + t) * kTileRows + j;
+                a.part[idx] = acc[mt][r];
+            }
+        }
+    }
+}
+
+// k assignment (the same for both operands): in the 64-k step at kk, MFMA
+// half h gives lane group g the 8 values kk + 32h + 8g .. +7, so the four
+// lanes of one row read 64 contiguous bytes per load.
+
+// Up to 16 tokens: one wavefront per 16-feature tile, activations read
+// straight from memory (a few KiB, cache resident).
 __global__ __launch_bounds__(64 * kWaves) void gemm_tiles_kernel(GemmArgs a) {
     const uint32_t lane = threadIdx.x & 63u;
     const uint32_t tile =
         blockIdx.x * kWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (tile >= a.num_tiles) return;
-
-    // matrix of this tile (uniform; constant-index selects keep the kernel
-    // arguments in scalar registers)
-    uint32_t start = 0, ksplit = 1, kchunk = 0, rows = 0, cols = 0;
-    uint64_t w_off = 0, part_off = 0;
-    const uint16_t *x = nullptr;
-    float *y = nullptr;
-#pragma unroll
-    for (uint32_t i = 0; i < kMax; ++i) {
-        if (i < a.n_mats && tile >= a.tile_start[i]) {
-            start = a.tile_start[i];
-            ksplit = a.ksplit[i];
-            kchunk = a.kchunk[i];
-            rows = a.rows[i];
-            cols = a.cols[i];
-            w_off = a.w_off[i];
-            part_off = a.part_off[i];
-            x = a.x[i];
-            y = a.y[i];
-        }
-    }
-    const uint32_t local = tile - start;
-    const uint32_t rb = local / ksplit;
-    const uint32_t s = local - rb * ksplit;
-    const uint32_t k0 = s * kchunk;
-    const uint32_t k1 = umin(cols, k0 + kchunk);
+    uint32_t first;
+    const Mat m = select_matrix(a, a.tile_start, tile, &first);
+    const uint32_t local = tile - first;
+    const uint32_t rb = local / m.ksplit;
+    const uint32_t s = local - rb * m.ksplit;
+    const uint32_t k0 = s * m.kchunk;
+    const uint32_t k1 = umin(m.cols, k0 + m.kchunk);
 
     const uint32_t j = lane & 15u;   // feature row (B) / token row (A) in the slice
     const uint32_t g = lane >> 4;    // k group
-    const uint16_t *wrow = a.w + w_off + static_cast<uint64_t>(rb * kTileRows + j) * cols + 16u * g;
+    const uint16_t *wrow = a.w + m.w_off + static_cast<uint64_t>(rb * kTileRows + j) * m.cols + 8u * g;
     // rows of x past the last token read token 0 and are masked to zero
-    const uint16_t *xrow[MT];
-    uint32_t xmask[MT];
-#pragma unroll
-    for (uint32_t mt = 0; mt < MT; ++mt) {
-        const uint32_t t = mt * 16u + j;
-        xmask[mt] = t < a.tokens ? ~0u : 0u;
-        xrow[mt] = x + static_cast<uint64_t>(t < a.tokens ? t : 0u) * cols + 16u * g;
-    }
+    const uint32_t xmask = j < a.tokens ? ~0u : 0u;
+    const uint16_t *xrow = m.x + static_cast<uint64_t>(j < a.tokens ? j : 0u) * m.cols + 8u * g;
 
-    f32x4 acc[MT];
-#pragma unroll
-    for (uint32_t mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    // one 64-k step: activations of every slice against the loaded weights
+    f32x4 acc[1] = {f32x4{0.f, 0.f, 0.f, 0.f}};
     auto step = [&](uint32_t kk, uint4 w0, uint4 w1) {
-#pragma unroll
-        for (uint32_t mt = 0; mt < MT; ++mt) {
-            const uint4 x0 = masked(load16(xrow[mt] + kk), xmask[mt]);
-            const uint4 x1 = masked(load16(xrow[mt] + kk + 8u), xmask[mt]);
-            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x0), as_bf16x8(w0), acc[mt],
-                                                              0, 0, 0);
-            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x1), as_bf16x8(w1), acc[mt],
-                                                              0, 0, 0);
-        }
+        const uint4 x0 = masked(load16(xrow + kk), xmask);
+        const uint4 x1 = masked(load16(xrow + kk + 32u), xmask);
+        acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x0), as_bf16x8(w0), acc[0], 0, 0, 0);
+        acc[0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x1), as_bf16x8(w1), acc[0], 0, 0, 0);
     };
     uint32_t k = k0;
     for (; k + kKPerIter <= k1; k += kKPerIter) {
@@ -146,31 +171,111 @@ __global__ __launch_bounds__(64 * kWaves) void gemm_tiles_kernel(GemmArgs a) {
 #pragma unroll
         for (uint32_t u = 0; u < kUnroll; ++u) {
             W[u][0] = load16(wrow + k + u * kKStep);
-            W[u][1] = load16(wrow + k + u * kKStep + 8u);
+            W[u][1] = load16(wrow + k + u * kKStep + 32u);
         }
 #pragma unroll
         for (uint32_t u = 0; u < kUnroll; ++u) step(k + u * kKStep, W[u][0], W[u][1]);
     }
-    for (; k < k1; k += kKStep) step(k, load16(wrow + k), load16(wrow + k + 8u));
+    for (; k < k1; k += kKStep) step(k, load16(wrow + k), load16(wrow + k + 32u));
+    write_tile<1>(a, m, rb, s, j, g, acc);
+}
 
-    // acc[mt][r] = sum over the range for token 16*mt + 4*g + r, feature
-    // rb*16 + j
-    const uint32_t feature = rb * kTileRows + j;
+// More than 16 tokens: a workgroup of kWaves waves covers 16*kWaves features
+// over one k range and stages the activations of each 256-k slab in LDS once
+// for all its waves (rows padded by 16 bytes so the 16 lanes of one read
+// pass hit distinct banks).  Weights still stream straight into registers.
+constexpr uint32_t kSlabK = kKPerIter;              // k per staged slab
+constexpr uint32_t kSlabStride = kSlabK * 2 + 16;   // bytes per token row in LDS
+
+template <uint32_t MT>
+__global__ __launch_bounds__(64 * kWaves) void gemm_slab_kernel(GemmArgs a) {
+    __shared__ __attribute__((aligned(16))) uint8_t slab[16 * MT * kSlabStride];
+    const uint32_t tid = threadIdx.x;
+    const uint32_t lane = tid & 63u;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t wgt = blockIdx.x;  // < num_wg by the grid size
+    uint32_t first;
+    const Mat m = select_matrix(a, a.wg_start, wgt, &first);
+    const uint32_t local = wgt - first;
+    const uint32_t rbw = local / m.ksplit;        // 64-feature block
+    const uint32_t s = local - rbw * m.ksplit;
+    const uint32_t k0 = s * m.kchunk;
+    const uint32_t k1 = umin(m.cols, k0 + m.kchunk);
+    const uint32_t rb = rbw * kWaves + wave;       // this wave's 16-feature tile
+    const bool active = rb * kTileRows < m.rows;   // uniform
+
+    const uint32_t j = lane & 15u;
+    const uint32_t g = lane >> 4;
+    const uint16_t *wrow =
+        a.w + m.w_off + static_cast<uint64_t>(active ? rb * kTileRows + j : 0u) * m.cols + 8u * g;
+
+    // slab loading: 16-byte piece q = tid + 64*kWaves*i covers token q/32,
+    // k offset 8*(q%32) of the slab
+    constexpr uint32_t kPieces = 16u * MT * (kSlabK / 8u);
+    constexpr uint32_t kPer = kPieces / (64u * kWaves);
+    uint4 xr[kPer];
+    auto load_slab = [&](uint32_t k) {
 #pragma unroll
-    for (uint32_t mt = 0; mt < MT; ++mt) {
+        for (uint32_t i = 0; i < kPer; ++i) {
+            const uint32_t q = tid + 64u * kWaves * i;
+            const uint32_t t = q >> 5, kk = k + 8u * (q & 31u);
+            const bool ok = t < a.tokens && kk < k1;
+            const uint4 v = load16(m.x + static_cast<uint64_t>(ok ? t : 0u) * m.cols + (ok ? kk : k0));
+            xr[i] = masked(v, ok ? ~0u : 0u);
+        }
+    };
+    auto store_slab = [&]() {
 #pragma unroll
-        for (uint32_t r = 0; r < 4; ++r) {
-            const uint32_t t = mt * 16u + 4u * g + r;
-            if (t >= a.tokens) continue;
-            if (ksplit == 1) {
-                y[static_cast<uint64_t>(t) * rows + feature] = acc[mt][r];
-            } else {
-                const uint64_t idx = part_off +
-                    (static_cast<uint64_t>(rb * ksplit + s) * a.tokens + t) * kTileRows + j;
-                a.part[idx] = acc[mt][r];
+        for (uint32_t i = 0; i < kPer; ++i) {
+            const uint32_t q = tid + 64u * kWaves * i;
+            *reinterpret_cast<uint4 *>(slab + (q >> 5) * kSlabStride + 16u * (q & 31u)) = xr[i];
+        }
+    };
+
+    f32x4 acc[MT];
+#pragma unroll
+    for (uint32_t mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    load_slab(k0);
+    store_slab();
+    __syncthreads();
+    for (uint32_t k = k0; k < k1; k += kSlabK) {
+        const uint32_t steps = umin(kUnroll, (k1 - k) / kKStep);  // uniform
+        uint4 W[kUnroll][2];
+        if (active) {
+#pragma unroll
+            for (uint32_t u = 0; u < kUnroll; ++u) {
+                const uint32_t kk = k + kKStep * umin(u, steps - 1u);  // in range
+                W[u][0] = load16(wrow + kk);
+                W[u][1] = load16(wrow + kk + 32u);
             }
         }
+        const bool more = k + kSlabK < k1;
+        if (more) load_slab(k + kSlabK);
+        if (active) {
+#pragma unroll
+            for (uint32_t u = 0; u < kUnroll; ++u) {
+                if (u < steps) {
+#pragma unroll
+                    for (uint32_t mt = 0; mt < MT; ++mt) {
+                        const uint8_t *row = slab + (16u * mt + j) * kSlabStride + 2u * (kKStep * u + 8u * g);
+                        const uint4 x0 = *reinterpret_cast<const uint4 *>(row);
+                        const uint4 x1 = *reinterpret_cast<const uint4 *>(row + 64u);
+                        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            as_bf16x8(x0), as_bf16x8(W[u][0]), acc[mt], 0, 0, 0);
+                        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                            as_bf16x8(x1), as_bf16x8(W[u][1]), acc[mt], 0, 0, 0);
+                    }
+                }
+            }
+        }
+        __syncthreads();  // every wave is done with this slab
+        if (more) {
+            store_slab();
+            __syncthreads();
+        }
     }
+    if (active) write_tile<MT>(a, m, rb, s, j, g, acc);
 }
 
 // y[t][f] = sum over k ranges s = 0, 1, ... of the partial sums, in that order.
@@ -258,7 +363,7 @@ int plan(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats, u
     r.part = static_cast<const float *>(workspace);
     g.n_mats = r.n_mats = n_mats;
     g.tokens = r.tokens = tokens;
-    uint64_t tiles = 0, part = 0, outs = 0;
+    uint64_t tiles = 0, wgs = 0, part = 0, outs = 0;
     for (uint32_t m = 0; m < n_mats; ++m) {
         const df11_matrix &d = mats[m];
         if (d.offset > n_weights || static_cast<uint64_t>(d.rows) * d.cols > n_weights - d.offset)
@@ -269,6 +374,7 @@ int plan(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats, u
         uint32_t ks, kc;
         split_of(d.cols, &ks, &kc);
         g.tile_start[m] = static_cast<uint32_t>(tiles);
+        g.wg_start[m] = static_cast<uint32_t>(wgs);
         g.ksplit[m] = r.ksplit[m] = ks;
         g.kchunk[m] = kc;
         g.rows[m] = r.rows[m] = d.rows;
@@ -279,6 +385,7 @@ int plan(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats, u
         g.y[m] = r.y[m] = y[m];
         r.out_start[m] = static_cast<uint32_t>(outs);
         tiles += static_cast<uint64_t>(d.rows / kTileRows) * ks;
+        wgs += static_cast<uint64_t>((d.rows + kTileRows * kWaves - 1) / (kTileRows * kWaves)) * ks;
         if (ks > 1) {
             part += static_cast<uint64_t>(d.rows) * ks * tokens;
             outs += static_cast<uint64_t>(d.rows) * tokens;
@@ -287,9 +394,11 @@ int plan(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats, u
     }
     for (uint32_t m = n_mats; m <= kMax; ++m) {
         g.tile_start[m] = static_cast<uint32_t>(tiles);
+        g.wg_start[m] = static_cast<uint32_t>(wgs);
         r.out_start[m] = static_cast<uint32_t>(outs);
     }
     g.num_tiles = static_cast<uint32_t>(tiles);
+    g.num_wg = static_cast<uint32_t>(wgs);
     r.total = static_cast<uint32_t>(outs);
     *gp = g;
     *rp = r;
@@ -298,12 +407,13 @@ int plan(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats, u
 
 int launch(const GemmArgs &g, const ReduceArgs &r, hipStream_t stream) {
     const uint32_t mt = (g.tokens + 15) / 16;
-    const dim3 grid((g.num_tiles + kWaves - 1) / kWaves), block(64 * kWaves);
+    const dim3 block(64 * kWaves);
+    const dim3 grid_tiles((g.num_tiles + kWaves - 1) / kWaves), grid_wg(g.num_wg);
     switch (mt) {
-    case 1: hipLaunchKernelGGL(gemm_tiles_kernel<1>, grid, block, 0, stream, g); break;
-    case 2: hipLaunchKernelGGL(gemm_tiles_kernel<2>, grid, block, 0, stream, g); break;
-    case 3: hipLaunchKernelGGL(gemm_tiles_kernel<3>, grid, block, 0, stream, g); break;
-    default: hipLaunchKernelGGL(gemm_tiles_kernel<4>, grid, block, 0, stream, g); break;
+    case 1: hipLaunchKernelGGL(gemm_tiles_kernel, grid_tiles, block, 0, stream, g); break;
+    case 2: hipLaunchKernelGGL(gemm_slab_kernel<2>, grid_wg, block, 0, stream, g); break;
+    case 3: hipLaunchKernelGGL(gemm_slab_kernel<3>, grid_wg, block, 0, stream, g); break;
+    default: hipLaunchKernelGGL(gemm_slab_kernel<4>, grid_wg, block, 0, stream, g); break;
     }
     if (hipGetLastError() != hipSuccess) return DF11_E_HIP;
     if (r.total) {
