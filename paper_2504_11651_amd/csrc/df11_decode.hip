@@ -333,8 +333,8 @@ __device__ __forceinline__ uint4 assemble_group(const uint8_t *buf, uint32_t g, 
 }
 
 // One 16-byte non-temporal store (the output is written once and not read
-// back by this kernel), or single-element stores for the elements of a group
-// that the block shares with its neighbour (elements k in [lo, hi)).
+// back by this kernel), or narrower stores for a group that the block shares
+// with its neighbour.
 __device__ __forceinline__ void store_group(const DecodeArgs &a, const Range &r, uint32_t g,
                                             const uint4 &o) {
     uint16_t *dst = a.out + r.g0 + (g << 3);
@@ -344,12 +344,20 @@ __device__ __forceinline__ void store_group(const DecodeArgs &a, const Range &r,
         __builtin_nontemporal_store(ov, reinterpret_cast<u32x4 *>(dst));
         return;
     }
+    // elements k in [lo, hi) of the group belong to this block: element
+    // pairs inside go out as one 4-byte store, a lone element as 2 bytes
     const int lo = static_cast<int>(r.shift) - static_cast<int>(g << 3);
     const int hi = static_cast<int>(r.lim) - static_cast<int>(g << 3);
     const uint32_t v[4] = {o.x, o.y, o.z, o.w};
 #pragma unroll
-    for (int k = 0; k < 8; ++k)
-        if (k >= lo && k < hi) dst[k] = static_cast<uint16_t>(v[k >> 1] >> ((k & 1) * 16));
+    for (int q = 0; q < 4; ++q) {
+        const bool in0 = 2 * q >= lo && 2 * q < hi, in1 = 2 * q + 1 >= lo && 2 * q + 1 < hi;
+        if (in0 && in1) {
+            reinterpret_cast<uint32_t *>(dst)[q] = v[q];
+        } else if (in0 || in1) {
+            dst[2 * q + (in1 ? 1 : 0)] = static_cast<uint16_t>(v[q] >> (in1 ? 16 : 0));
+        }
+    }
 }
 
 // Assemble and store every group of the block: groups first + k*step.  The
