@@ -314,6 +314,22 @@ def main() -> int:
         torch.cuda.synchronize()
         del src, dst
 
+    # context: what a plain device-to-device copy (read + write, no decode)
+    # sustains on this GPU, 512 MiB each way (twice the last-level cache),
+    # same event timing
+    src = torch.empty(1 << 29, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(20):
+        dst.copy_(src)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_gbs = 2.0 * src.numel() * 20 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del src, dst
+
     z = hs.sizes
     exp_bytes_exact = (int(z.total_bits) + 7) // 8
     read_bytes = exp_bytes_exact + n + int(z.gap_bytes) + int(z.block_pos_bytes) + \
@@ -357,6 +373,8 @@ def main() -> int:
             "traffic": None if traffic is None else round(traffic),
         },
         "pct_hbm_roofline": round(100.0 * achieved / HBM_PEAK_GBS, 2),
+        "device_copy_gbs": round(copy_gbs, 1),
+        "achieved_over_device_copy": round(achieved / copy_gbs, 4),
         "weights_per_s": round(n / (ms_per_step * 1e-3), 1),
         "bit_exact": bit_exact,
         "kernel_ms": {"mean_in_timed_region": round(kern_ms, 5),

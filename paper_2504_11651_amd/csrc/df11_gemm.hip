@@ -187,8 +187,11 @@ __global__ __launch_bounds__(64 * kWaves) void gemm_tiles_kernel(GemmArgs a) {
 constexpr uint32_t kSlabK = kKPerIter;              // k per staged slab
 constexpr uint32_t kSlabStride = kSlabK * 2 + 16;   // bytes per token row in LDS
 
+// (4 waves per SIMD: the accumulators then stay in VGPRs, which the compiler
+// otherwise spills to AGPRs at 3 waves per SIMD)
 template <uint32_t MT>
-__global__ __launch_bounds__(64 * kWaves) void gemm_slab_kernel(GemmArgs a) {
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(4))) void
+gemm_slab_kernel(GemmArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t slab[16 * MT * kSlabStride];
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
@@ -209,16 +212,18 @@ __global__ __launch_bounds__(64 * kWaves) void gemm_slab_kernel(GemmArgs a) {
     const uint16_t *wrow =
         a.w + m.w_off + static_cast<uint64_t>(active ? rb * kTileRows + j : 0u) * m.cols + 8u * g;
 
-    // slab loading: 16-byte piece q = tid + 64*kWaves*i covers token q/32,
-    // k offset 8*(q%32) of the slab
-    constexpr uint32_t kPieces = 16u * MT * (kSlabK / 8u);
+    // slab loading: 16-byte piece q = tid + 64*kWaves*i covers token
+    // q / kRowPieces, k offset 8 * (q % kRowPieces) of the slab
+    constexpr uint32_t kRowPieces = kSlabK / 8u;
+    constexpr uint32_t kPieces = 16u * MT * kRowPieces;
     constexpr uint32_t kPer = kPieces / (64u * kWaves);
+    static_assert(kPieces % (64u * kWaves) == 0, "whole pieces per thread");
     uint4 xr[kPer];
     auto load_slab = [&](uint32_t k) {
 #pragma unroll
         for (uint32_t i = 0; i < kPer; ++i) {
             const uint32_t q = tid + 64u * kWaves * i;
-            const uint32_t t = q >> 5, kk = k + 8u * (q & 31u);
+            const uint32_t t = q / kRowPieces, kk = k + 8u * (q % kRowPieces);
             const bool ok = t < a.tokens && kk < k1;
             const uint4 v = load16(m.x + static_cast<uint64_t>(ok ? t : 0u) * m.cols + (ok ? kk : k0));
             xr[i] = masked(v, ok ? ~0u : 0u);
@@ -228,7 +233,8 @@ __global__ __launch_bounds__(64 * kWaves) void gemm_slab_kernel(GemmArgs a) {
 #pragma unroll
         for (uint32_t i = 0; i < kPer; ++i) {
             const uint32_t q = tid + 64u * kWaves * i;
-            *reinterpret_cast<uint4 *>(slab + (q >> 5) * kSlabStride + 16u * (q & 31u)) = xr[i];
+            *reinterpret_cast<uint4 *>(slab + (q / kRowPieces) * kSlabStride + 16u * (q % kRowPieces)) =
+                xr[i];
         }
     };
 
