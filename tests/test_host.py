@@ -326,3 +326,21 @@ def test_decode_rejects_bad_descriptors_without_launching():
     st = hs.struct()
     st.sizes.n_elems = 0  # nothing to do: no launch, ok
     assert codec.lib().df11_decode_block(ctypes.byref(st), None, None) == 0
+
+
+def test_size_limits_of_32_bit_positions():
+    # BlockOutputPos entries are 32-bit: a stream of more than 2^32 - 1
+    # weights is refused when sized, and a descriptor claiming one is
+    # refused by the decoder before anything is launched
+    counts = np.zeros(256, np.uint64)
+    counts[120], counts[121] = 2 ** 31, 2 ** 31  # 2^32 weights
+    cb = codec.codebook_from_counts(counts)
+    with pytest.raises(codec.DF11Error) as e:
+        codec.encoded_sizes(cb, codec.make_layout())
+    assert e.value.rc == -1
+    counts[121] -= 1  # 2^32 - 1 weights: allowed
+    z = codec.encoded_sizes(codec.codebook_from_counts(counts), codec.make_layout())
+    assert z.n_elems == 2 ** 32 - 1
+    st = _fresh().struct()
+    st.sizes.n_elems = 2 ** 32
+    assert codec.lib().df11_decode_block(ctypes.byref(st), None, None) == -1
