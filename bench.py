@@ -340,6 +340,7 @@ def main() -> int:
     ms_per_step = wall * 1e3 / args.steps
     value = 2.0 * n / (ms_per_step * 1e-3) / 1e9
     grid, block, lds = codec.launch_shape(ds)
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
     traffic = profiled_traffic(args.workload, lay)
 
     rec = {
@@ -362,7 +363,8 @@ def main() -> int:
             "layout": {"bytes_per_thread": int(lay.bytes_per_thread),
                        "threads_per_block": int(lay.threads_per_block),
                        "lut_bits": int(lay.lut_bits)},
-            "launch": {"grid": grid, "block": block, "lds_bytes": lds},
+            "launch": {"grid": grid, "block": block, "lds_bytes": lds,
+                       "waves_per_simd": round(grid * block / 64 / (4 * cus), 2)},
         },
         "roofline": {
             "bound": "hbm",
