@@ -512,6 +512,7 @@ std::mutex g_mu;
 std::vector<DeviceInfo> g_dev;
 
 constexpr uint32_t kWaveChoices[4] = {4, 8, 12, 16};
+constexpr size_t kMaxShapes = 64;  // cached launch shapes per device
 
 KernelFn wave_kernel(uint32_t W) {
     switch (W) {
@@ -633,6 +634,7 @@ int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *bloc
             if (pc < 1) return DF11_E_UNSUPPORTED;
             ls.per_cu = static_cast<uint32_t>(pc);
         }
+        if (di.shapes.size() >= kMaxShapes) di.shapes.clear();  // bounded lookup cost
         di.shapes.push_back(ls);
         found = &di.shapes.back();
     }
