@@ -215,6 +215,30 @@ int df11_block_forward(const df11_stream *dev, uint16_t *weights_out, const df11
                        float *const *y, void *workspace, uint64_t workspace_bytes,
                        hipStream_t stream);
 
+/* ---- Fused decode-and-multiply for one token (decode-time products without
+ * a decoded copy of the block: the decompression of Algorithm 1 feeds the
+ * products of Sec. 2.3.3 directly, so the BF16 weights never reach memory).
+ *
+ * For every matrix m: y[m][r] = sum_k x[m][k] * W_m[r][k] with one
+ * activation row, BF16 products accumulated in fp32 (bf16 dot-product
+ * instructions), W_m decoded from the stream on chip.
+ *   dev:       device stream, layout with threads_per_block = 64;
+ *   mats:      host array of n_mats (1..DF11_MAX_MATRICES) descriptors, sorted
+ *              by offset and disjoint, inside [0, n_elems); each with cols a
+ *              multiple of 64 and >= 2048, offset a multiple of 8, and at
+ *              least 4096 weights;
+ *   x:         host array of device pointers, x[m] = cols_m BF16, 16-byte aligned;
+ *   y:         host array of device pointers, y[m] = rows_m fp32, 4-byte aligned;
+ *   workspace: device, >= df11_gemv_workspace_bytes, 16-byte aligned.
+ * The summation order is fixed by the stream's blocks (deterministic; it is
+ * not the order df11_block_gemm uses, so results agree with it to rounding,
+ * not bit for bit).  Enqueued on `stream`.  DF11_E_UNSUPPORTED for shapes or
+ * layouts outside the requirements above. */
+int df11_gemv_workspace_bytes(const df11_stream *dev, uint64_t *bytes);
+int df11_block_gemv(const df11_stream *dev, const df11_matrix *mats, uint32_t n_mats,
+                    const uint16_t *const *x, float *const *y, void *workspace,
+                    uint64_t workspace_bytes, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *df11_strerror(int status);
 

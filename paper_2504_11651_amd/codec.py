@@ -26,7 +26,8 @@ ERRORS = {
 EXPORTS = (
     "df11_build_codebook", "df11_codebook_from_counts", "df11_encoded_sizes", "df11_encode",
     "df11_build_tables", "df11_validate", "df11_decode_block", "df11_decode_launch_shape",
-    "df11_gemm_workspace_bytes", "df11_block_gemm", "df11_block_forward", "df11_strerror",
+    "df11_gemm_workspace_bytes", "df11_block_gemm", "df11_block_forward",
+    "df11_gemv_workspace_bytes", "df11_block_gemv", "df11_strerror",
 )
 
 MAX_MATRICES = 8  # DF11_MAX_MATRICES
@@ -117,6 +118,8 @@ def lib():
                             vp, u64, vp],
         "df11_block_forward": [P(Stream), vp, P(Matrix), ctypes.c_uint32, P(vp), ctypes.c_uint32,
                                P(vp), vp, u64, vp],
+        "df11_gemv_workspace_bytes": [P(Stream), P(u64)],
+        "df11_block_gemv": [P(Stream), P(Matrix), ctypes.c_uint32, P(vp), P(vp), vp, u64, vp],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -359,4 +362,38 @@ def block_forward(ds: DeviceStream, weights_out, mats, xs, ys, workspace=None, s
                                     tokens, yp, ctypes.c_void_p(ws_ptr), ws_bytes,
                                     ctypes.c_void_p(_handle(stream, ds.device))),
            "df11_block_forward")
+    return ys
+
+
+# ------------------------------------------------ fused decode-and-multiply
+def gemv_workspace_bytes(ds: DeviceStream) -> int:
+    """Workspace bytes block_gemv needs for this stream."""
+    out = ctypes.c_uint64()
+    _check(lib().df11_gemv_workspace_bytes(ctypes.byref(ds.struct()), ctypes.byref(out)),
+           "df11_gemv_workspace_bytes")
+    return int(out.value)
+
+
+def block_gemv(ds: DeviceStream, mats, xs, ys, workspace=None, stream=None):
+    """ys[m][r] = sum_k xs[m][k] * W_m[r][k] for one token, with the weights of
+    ``ds`` decoded on chip (never written out).  xs[m]: bf16 (cols,) or
+    (1, cols); ys[m]: fp32 (rows,) or (1, rows)."""
+    import torch
+    if not (len(mats) == len(xs) == len(ys)):
+        raise ValueError("one activation and one output tensor per matrix")
+    for (off, rows, cols), x, y in zip(mats, xs, ys):
+        if x.numel() != cols or x.element_size() != 2 or not x.is_contiguous():
+            raise ValueError("x[m] must be a contiguous bf16 tensor of cols elements")
+        if y.numel() != rows or y.element_size() != 4 or not y.is_contiguous():
+            raise ValueError("y[m] must be a contiguous fp32 tensor of rows elements")
+    if workspace is None:
+        workspace = torch.empty(max(gemv_workspace_bytes(ds) // 4, 4), dtype=torch.float32,
+                                device=ds.device)
+    xp = (ctypes.c_void_p * len(xs))(*[x.data_ptr() for x in xs])
+    yp = (ctypes.c_void_p * len(ys))(*[y.data_ptr() for y in ys])
+    _check(lib().df11_block_gemv(ctypes.byref(ds.struct()), _mats(mats), len(mats), xp, yp,
+                                 ctypes.c_void_p(workspace.data_ptr()),
+                                 workspace.numel() * workspace.element_size(),
+                                 ctypes.c_void_p(_handle(stream, ds.device))),
+           "df11_block_gemv")
     return ys

@@ -1,0 +1,405 @@
+// Building blocks of the DFloat11 decoder shared by the kernels that decode
+// a stream (Algorithm 1 of arXiv 2504.11651): stream loads, table lookups,
+// the two decode phases, the wave prefix sum and BF16 assembly, plus the
+// host-side descriptor check.  Included by the decode kernels and by the
+// fused decode-and-multiply kernel.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "df11.h"
+#include "df11_tables.h"
+
+namespace df11dec {
+
+
+constexpr uint32_t kScanSlots = 16;  // waves per workgroup (<= 1024 threads)
+// Exponent buffer bytes past the largest block: alignment shift (< 8), codes
+// decoded past a block's end, and the 4 bytes per kept lookup that a lane may
+// store past a clamped start offset.
+constexpr uint32_t kBufSlack = 128;
+
+struct DecodeArgs {
+    const uint8_t *exp;
+    const uint8_t *sm;
+    const uint32_t *gaps;      // packed Gaps read as 32-bit words
+    const uint32_t *block_pos; // B + 1 entries
+    const uint8_t *tables;     // LDS image (blob past its header)
+    uint16_t *out;
+    uint64_t total_bits;
+    uint32_t n_elems;
+    uint32_t num_chunks;
+    uint32_t num_blocks;
+    uint32_t lut_bits;
+    uint32_t max_len;
+    uint32_t table_lds_bytes;
+    uint32_t buf_bytes;        // exponent buffer, multiple of 16
+};
+
+__device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b ? a : b; }
+__device__ __forceinline__ uint32_t umax(uint32_t a, uint32_t b) { return a > b ? a : b; }
+
+// 4 stream bytes as loaded (little endian) -> word whose bit j is stream bit j
+// (the stream is most-significant-bit first within each byte).
+__device__ __forceinline__ uint32_t lsb_first(uint32_t le) {
+    return __builtin_bitreverse32(__builtin_bswap32(le));
+}
+
+// 32 bits starting at bit p (0 <= p < 64) of the 96 bits w0:w1:w2.
+__device__ __forceinline__ uint32_t window_at(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t p) {
+    const bool upper = p >= 32;
+    const uint32_t lo = upper ? w1 : w0;
+    const uint32_t hi = upper ? w2 : w1;
+    return __builtin_amdgcn_alignbit(hi, lo, p);
+}
+
+// The kernels declare no static LDS, so the dynamically sized LDS (and the
+// decode table at its start) begins at group-segment offset 0; table entries
+// are read through LDS byte offsets.
+__device__ __forceinline__ uint2 lds_entry(uint32_t byte_offset) {
+    const uint64_t v = *(__attribute__((address_space(3))) const uint64_t *)
+        static_cast<uintptr_t>(byte_offset);
+    return make_uint2(static_cast<uint32_t>(v), static_cast<uint32_t>(v >> 32));
+}
+
+struct Tables {
+    // K-bit entries (8 bytes: x = exponents, y = meta) at LDS offset 0
+    const uint32_t *lj_last; // [33]
+    const uint32_t *offset;  // [33]
+    const uint8_t *sorted;   // [256]
+    uint32_t addr_mask;      // (2^K - 1) << 3: entry byte offset from a shifted window
+    uint32_t lut_bits;
+    uint32_t max_len;
+};
+
+__device__ __forceinline__ Tables stage_tables(const DecodeArgs &a, uint8_t *lds) {
+    Tables tb;
+    const uint32_t ent_bytes = 8u << a.lut_bits;
+    tb.lj_last = reinterpret_cast<const uint32_t *>(lds + ent_bytes);
+    tb.offset = tb.lj_last + 33;
+    tb.sorted = reinterpret_cast<const uint8_t *>(tb.offset + 33);
+    tb.addr_mask = ((1u << a.lut_bits) - 1u) << 3;
+    tb.lut_bits = a.lut_bits;
+    tb.max_len = a.max_len;
+    return tb;
+}
+
+// Code longer than the table index: canonical length search on the
+// left-justified window, then rank within the length.
+__device__ __forceinline__ uint2 decode_long(const Tables &t, uint32_t win) {
+    const uint32_t v = __builtin_bitreverse32(win);
+    uint32_t L = t.lut_bits + 1;
+    while (L < t.max_len && v > t.lj_last[L]) ++L;
+    const uint32_t idx = ((v >> (32u - L)) + t.offset[L]) & 255u;
+    return make_uint2(t.sorted[idx], L | (1u << 8) | (1u << 16));
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave: four row shifts give the
+// sums within each row of 16 lanes, two row broadcasts carry row totals.
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t v) {
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x111, 0xF, 0xF, true));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x112, 0xF, 0xF, true));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x114, 0xF, 0xF, true));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x118, 0xF, 0xF, true));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x142, 0xA, 0xF, false));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x143, 0xC, 0xF, false));
+    return v;
+}
+
+// Orders this wave's LDS accesses (other lanes' writes become visible to
+// later reads: LDS executes a wave's instructions in order; this keeps the
+// compiler from moving accesses across).
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// 4 sign/mantissa bytes + 4 exponents -> 4 BF16 (two words, low element first).
+__device__ __forceinline__ void assemble4(uint32_t S, uint32_t E, uint32_t &o0, uint32_t &o1) {
+    const uint32_t lo = (S & 0x7F7F7F7Fu) | ((E << 7) & 0x80808080u);  // (e&1)<<7 | mantissa
+    const uint32_t hi = (S & 0x80808080u) | ((E >> 1) & 0x7F7F7F7Fu);  // sign<<7 | e>>1
+    o0 = __builtin_amdgcn_perm(hi, lo, 0x05010400u);
+    o1 = __builtin_amdgcn_perm(hi, lo, 0x07030602u);
+}
+
+// Raw global words one lane needs for chunk c of block b: the chunk's 8
+// bytes, the next 4 bytes, the two 32-bit words holding Gaps[c] and
+// Gaps[c+1], and the block's two BlockOutputPos entries.
+struct ChunkWords {
+    uint32_t x, y, z, g0, g1, bp0, bp1;
+};
+
+__device__ __forceinline__ ChunkWords load_chunk(const DecodeArgs &a, uint32_t b, uint32_t c) {
+    ChunkWords r;
+    r.bp0 = a.block_pos[b];
+    r.bp1 = a.block_pos[b + 1];
+    const uint2 own = *reinterpret_cast<const uint2 *>(a.exp + 8ull * c);
+    r.x = own.x;
+    r.y = own.y;
+    r.z = *reinterpret_cast<const uint32_t *>(a.exp + 8ull * c + 8);
+    const uint64_t gw = (5ull * c) >> 5;
+    r.g0 = a.gaps[gw];
+    r.g1 = a.gaps[gw + 1];
+    return r;
+}
+
+// Lookups kept in registers between the count phase and the write phase;
+// a chunk needing more (short codes, 4 per lookup) continues in a loop.
+constexpr int kKeep = 10;
+// 8-element output groups whose sign/mantissa bytes are fetched at block start.
+constexpr int kPre = 4;
+
+// One chunk's decode state.  w*: the chunk's bits (word j bit i = stream bit
+// 32j+i); s*: the same bits moved up by 3, so that a window taken from s* at
+// bit p holds stream bits p.. at bits 3.. and masking it gives the byte
+// offset of the table entry directly.
+struct Chunk {
+    uint32_t w0, w1, w2, s0, s1, s2, start, end;
+};
+
+__device__ __forceinline__ Chunk chunk_setup(const DecodeArgs &a, const ChunkWords &cw, uint32_t c) {
+    Chunk ch;
+    ch.w0 = lsb_first(cw.x);
+    ch.w1 = lsb_first(cw.y);
+    ch.w2 = lsb_first(cw.z);
+    ch.s0 = ch.w0 << 3;
+    ch.s1 = __builtin_amdgcn_alignbit(ch.w1, ch.w0, 29);
+    ch.s2 = __builtin_amdgcn_alignbit(ch.w2, ch.w1, 29);
+    const uint64_t gv = ((static_cast<uint64_t>(__builtin_bswap32(cw.g0)) << 32) |
+                         __builtin_bswap32(cw.g1))
+                        << ((5u * c) & 31u);
+    const uint32_t gap_own = static_cast<uint32_t>(gv >> 59);
+    const uint32_t gap_next = static_cast<uint32_t>(gv >> 54) & 31u;
+    ch.start = 0;
+    ch.end = 0;
+    if (c < a.num_chunks) {
+        ch.start = gap_own;
+        const uint32_t e = (c + 1 < a.num_chunks) ? 64u + gap_next
+                                                  : static_cast<uint32_t>(a.total_bits - 64ull * c);
+        ch.end = min(e, 95u);
+    }
+    return ch;
+}
+
+__device__ __forceinline__ uint2 lookup(const Tables &t, const Chunk &ch, uint32_t p) {
+    const uint32_t ws = window_at(ch.s0, ch.s1, ch.s2, p);
+    uint2 e = lds_entry(ws & t.addr_mask);
+    if (e.y == 0u) e = decode_long(t, window_at(ch.w0, ch.w1, ch.w2, p));
+    return e;
+}
+
+// Phase 1: decode the codes that start in the chunk, keep up to kKeep
+// lookups (exponent words in sy, code counts one byte each in npk), and
+// count the codes.  Returns the count; *p_rest = where decoding stopped.
+__device__ __forceinline__ uint32_t decode_count(const Tables &t, const Chunk &ch,
+                                                 uint32_t (&sy)[kKeep],
+                                                 uint32_t (&npk)[(kKeep + 3) / 4],
+                                                 uint32_t *p_rest) {
+#pragma unroll
+    for (int k = 0; k < (kKeep + 3) / 4; ++k) npk[k] = 0u;
+    uint32_t p = ch.start, cnt = 0, last_p = 0, last_meta = 0;
+#pragma unroll
+    for (int k = 0; k < kKeep; ++k) {
+        const bool act = p < ch.end;
+        sy[k] = 0u;
+        if (__builtin_amdgcn_ballot_w64(act) == 0) continue;  // wave-uniform skip
+        const uint32_t ws = window_at(ch.s0, ch.s1, ch.s2, p);
+        uint2 e = lds_entry(ws & t.addr_mask);
+        if (act && e.y == 0u) e = decode_long(t, window_at(ch.w0, ch.w1, ch.w2, p));
+        const uint32_t m = act ? e.y : 0u;
+        sy[k] = e.x;
+        constexpr uint32_t sel[4] = {0x03020105u, 0x03020500u, 0x03050100u, 0x05020100u};
+        npk[k / 4] = __builtin_amdgcn_perm(m, npk[k / 4], sel[k % 4]);  // byte k%4 <- count
+        last_p = act ? p : last_p;
+        last_meta = act ? m : last_meta;
+        p += e.y & 0xFFu;  // done lanes only move further past `end`
+        cnt += (m >> 8) & 0xFFu;
+    }
+    *p_rest = p;
+    for (uint32_t it = 0; p < ch.end && it < 96u; ++it) {
+        const uint2 e = lookup(t, ch, p);
+        last_p = p;
+        last_meta = e.y;
+        p += e.y & 0xFFu;
+        cnt += (e.y >> 8) & 0xFFu;
+    }
+    // codes of the last lookup that start at or past `end` belong to the next chunk
+    return cnt - __builtin_popcount((last_meta >> 16) >> min(ch.end - last_p, 31u));
+}
+
+// OR 4 exponent bytes into the zeroed buffer at byte offset off.
+__device__ __forceinline__ void or_exponents(uint32_t *buf32, uint32_t off, uint32_t syms) {
+    const uint64_t v = static_cast<uint64_t>(syms) << ((off & 3u) << 3);
+    atomicOr(&buf32[off >> 2], static_cast<uint32_t>(v));
+    atomicOr(&buf32[(off >> 2) + 1], static_cast<uint32_t>(v >> 32));
+}
+
+// Phase 2: exponents into the LDS buffer at output offset off (the kept
+// lookups, then the rest of a long chunk by decoding again).  A valid entry
+// holds at most 4 codes, so 3 bits of each kept count suffice; with the start
+// clamped, the kept lookups stay inside the buffer whatever the metadata and
+// tables hold; the rest are clamped one by one.
+__device__ __forceinline__ void emit_exponents(const Tables &t, const Chunk &ch,
+                                               const uint32_t (&sy)[kKeep],
+                                               const uint32_t (&npk)[(kKeep + 3) / 4],
+                                               uint32_t p_rest, uint32_t off, uint32_t *buf32,
+                                               uint32_t cap_bytes) {
+    off = umin(off, cap_bytes - 8u * kKeep);
+#pragma unroll
+    for (int k = 0; k < kKeep; ++k) {
+        const uint32_t n = (npk[k / 4] >> (8 * (k % 4))) & 7u;
+        if (n != 0u) {
+            or_exponents(buf32, off, sy[k]);
+            off += n;
+        }
+    }
+    uint32_t p = p_rest;
+    for (uint32_t it = 0; p < ch.end && it < 96u; ++it) {
+        const uint2 e = lookup(t, ch, p);
+        off = umin(off, cap_bytes);
+        or_exponents(buf32, off, e.x);
+        off += (e.y >> 8) & 0xFFu;
+        p += e.y & 0xFFu;
+    }
+}
+
+// A block's output range, clamped to the buffer and the tensor.
+struct Range {
+    uint32_t s, shift, lim, g0, ngroups;
+};
+
+__device__ __forceinline__ Range block_range(const DecodeArgs &a, const ChunkWords &cw) {
+    Range r;
+    r.s = umin(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(cw.bp0)), a.n_elems);
+    uint32_t e = umax(umin(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(cw.bp1)), a.n_elems), r.s);
+    e = umin(e, r.s + (a.buf_bytes - kBufSlack));
+    r.shift = r.s & 7u;
+    r.lim = r.shift + (e - r.s);
+    r.g0 = r.s - r.shift;
+    r.ngroups = (r.lim + 7u) >> 3;
+    return r;
+}
+
+__device__ __forceinline__ bool full_group(const Range &r, uint32_t g) {
+    return (g << 3) >= r.shift && (g << 3) + 8u <= r.lim;
+}
+
+// Sign/mantissa bytes of groups first, first+step, ... (kPre of them).  The
+// buffer is zero padded past n_elems to a multiple of 16 bytes, so a whole
+// group can be read even where the block starts or ends inside it.
+__device__ __forceinline__ void prefetch_sm(const DecodeArgs &a, const Range &r, uint32_t first,
+                                            uint32_t step, uint2 (&S)[kPre]) {
+    const uint32_t last = umax(r.ngroups, 1u) - 1u;  // groups past the block reread its last one
+#pragma unroll
+    for (int k = 0; k < kPre; ++k) {
+        const uint32_t g = umin(first + k * step, last);
+        S[k] = *reinterpret_cast<const uint2 *>(a.sm + r.g0 + (g << 3));
+    }
+}
+
+// 8 outputs of group g from its sign/mantissa bytes and the exponent buffer.
+__device__ __forceinline__ uint4 assemble_group(const uint8_t *buf, uint32_t g, uint2 Sg) {
+    const uint2 E = reinterpret_cast<const uint2 *>(buf)[g];
+    uint4 o;
+    assemble4(Sg.x, E.x, o.x, o.y);
+    assemble4(Sg.y, E.y, o.z, o.w);
+    return o;
+}
+
+// One 16-byte non-temporal store (the output is written once and not read
+// back by this kernel), or narrower stores for a group that the block shares
+// with its neighbour.
+__device__ __forceinline__ void store_group(const DecodeArgs &a, const Range &r, uint32_t g,
+                                            const uint4 &o) {
+    uint16_t *dst = a.out + r.g0 + (g << 3);
+    if (full_group(r, g)) {
+        typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4 ov = {o.x, o.y, o.z, o.w};
+        __builtin_nontemporal_store(ov, reinterpret_cast<u32x4 *>(dst));
+        return;
+    }
+    // elements k in [lo, hi) of the group belong to this block: element
+    // pairs inside go out as one 4-byte store, a lone element as 2 bytes
+    const int lo = static_cast<int>(r.shift) - static_cast<int>(g << 3);
+    const int hi = static_cast<int>(r.lim) - static_cast<int>(g << 3);
+    const uint32_t v[4] = {o.x, o.y, o.z, o.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const bool in0 = 2 * q >= lo && 2 * q < hi, in1 = 2 * q + 1 >= lo && 2 * q + 1 < hi;
+        if (in0 && in1) {
+            reinterpret_cast<uint32_t *>(dst)[q] = v[q];
+        } else if (in0 || in1) {
+            dst[2 * q + (in1 ? 1 : 0)] = static_cast<uint16_t>(v[q] >> (in1 ? 16 : 0));
+        }
+    }
+}
+
+// Assemble and store every group of the block: groups first + k*step.  The
+// first kPre use the bytes fetched when the block started.  Loads and stores
+// share one in-order counter on this GPU, so all of those groups are
+// assembled (their loads waited for) before the first store is issued;
+// otherwise each wait would also wait for the stores issued before it.
+__device__ __forceinline__ void assemble_block(const DecodeArgs &a, const Range &r,
+                                               const uint8_t *buf, uint32_t first, uint32_t step,
+                                               const uint2 (&S)[kPre]) {
+    uint4 O[kPre];
+#pragma unroll
+    for (int k = 0; k < kPre; ++k) {
+        const uint32_t g = first + k * step;
+        O[k] = make_uint4(0u, 0u, 0u, 0u);
+        if (g < r.ngroups) O[k] = assemble_group(buf, g, S[k]);
+    }
+#pragma unroll
+    for (int k = 0; k < kPre; ++k) {
+        const uint32_t g = first + k * step;
+        if (g < r.ngroups) store_group(a, r, g, O[k]);
+    }
+    for (uint32_t g = first + kPre * step; g < r.ngroups; g += step)
+        store_group(a, r, g,
+                    assemble_group(buf, g, *reinterpret_cast<const uint2 *>(a.sm + r.g0 + (g << 3))));
+}
+
+__device__ __forceinline__ void stage_table_blob(const DecodeArgs &a, uint8_t *lds, uint32_t tid,
+                                                 uint32_t nthreads) {
+    const uint4 *src = reinterpret_cast<const uint4 *>(a.tables);
+    uint4 *dst = reinterpret_cast<uint4 *>(lds);
+    for (uint32_t i = tid; i < (a.table_lds_bytes >> 4); i += nthreads) dst[i] = src[i];
+}
+
+// ---- host side ------------------------------------------------------------
+
+inline bool layout_supported(uint32_t T) {
+    return T == 64 || T == 128 || T == 256 || T == 512 || T == 1024;
+}
+
+inline uint32_t buf_bytes_for(uint32_t max_elems) {
+    return (max_elems + kBufSlack + 15u) & ~15u;
+}
+
+inline int check_stream(const df11_stream *s) {
+    if (!s) return DF11_E_INVALID_ARG;
+    const df11_sizes &z = s->sizes;
+    if (s->layout.bytes_per_thread != 8) return DF11_E_UNSUPPORTED;
+    if (!layout_supported(s->layout.threads_per_block)) return DF11_E_UNSUPPORTED;
+    if (s->layout.lut_bits < 8 || s->layout.lut_bits > 12) return DF11_E_INVALID_ARG;
+    if (z.n_elems == 0) return DF11_OK;
+    if (!s->exp || !s->sm || !s->gaps || !s->block_pos || !s->tables) return DF11_E_INVALID_ARG;
+    if (z.n_elems > 0xFFFFFFFFull || z.num_blocks > 0xFFFFFFFFull / 1024) return DF11_E_INVALID_ARG;
+    if (z.max_code_len > 32 || z.table_bytes != df11tab::blob_bytes(s->layout.lut_bits))
+        return DF11_E_INVALID_ARG;
+    const uint64_t T = s->layout.threads_per_block;
+    if (z.exp_bytes < z.num_blocks * 8 * T + 16) return DF11_E_INVALID_ARG;
+    if (z.gap_bytes < 4 * ((5 * (z.num_blocks * T + 1) + 31) / 32 + 2)) return DF11_E_INVALID_ARG;
+    if (z.num_chunks > z.num_blocks * T) return DF11_E_INVALID_ARG;
+    if (z.max_elems_per_block > 64u * T) return DF11_E_INVALID_ARG;
+    if (z.sm_bytes < ((z.n_elems + 15) & ~uint64_t{15}) + 16) return DF11_E_INVALID_ARG;
+    if ((reinterpret_cast<uintptr_t>(s->sm) & 15u) || (reinterpret_cast<uintptr_t>(s->exp) & 7u) ||
+        (reinterpret_cast<uintptr_t>(s->gaps) & 3u) || (reinterpret_cast<uintptr_t>(s->tables) & 15u) ||
+        (reinterpret_cast<uintptr_t>(s->block_pos) & 3u))
+        return DF11_E_INVALID_ARG;
+    return DF11_OK;
+}
+
+}  // namespace df11dec

@@ -3,6 +3,7 @@ and argument validation.  Every call here is rejected before anything is
 enqueued, so no device is touched (the pointers are never dereferenced)."""
 import ctypes
 
+import numpy as np
 import pytest
 
 from paper_2504_11651_amd import codec, synth
@@ -94,3 +95,77 @@ def test_block_forward_checks_gemm_arguments_before_decoding():
     assert rc == -1
     assert L.df11_block_forward(None, ctypes.c_void_p(A), m, 1, xp, 1, yp, ctypes.c_void_p(0), 0,
                                 ctypes.c_void_p(0)) == -1
+
+
+# ---- fused decode-and-multiply: argument checks (rejected before launch)
+def _stream_desc(n=1 << 20, T=64):
+    st = codec.Stream()
+    st.sizes.n_elems = n
+    st.sizes.num_blocks = 4
+    st.layout.bytes_per_thread, st.layout.threads_per_block, st.layout.lut_bits = 8, T, 11
+    return st
+
+
+def _call_gemv(st, mats, xs, ys, ws, ws_bytes):
+    L = codec.lib()
+    m = codec._mats(mats)
+    xp = (ctypes.c_void_p * len(xs))(*xs)
+    yp = (ctypes.c_void_p * len(ys))(*ys)
+    return L.df11_block_gemv(ctypes.byref(st), m, len(mats), xp, yp, ctypes.c_void_p(ws),
+                             ws_bytes, ctypes.c_void_p(0))
+
+
+@pytest.mark.parametrize("mats,rc", [
+    ([(0, 16, 1024)], -6),                  # fewer than 2048 columns
+    ([(0, 4, 2048 + 32)], -6),              # columns not a multiple of 64
+    ([(8, 1, 2048)], -6),                   # fewer than 4096 weights
+    ([(4, 16, 2048)], -6),                  # offset not 16-byte aligned
+    ([(65536, 16, 2048), (0, 16, 2048)], -6),  # not sorted by offset
+    ([(0, 16, 2048), (16 * 2048 - 8, 16, 2048)], -6),  # overlapping
+    ([(0, 1024, 2048)], -1),                # past the end of the stream
+])
+def test_gemv_shape_rejections(mats, rc):
+    st = _stream_desc()
+    # null stream buffers make check_stream fail first for a non-empty
+    # stream, so give them stand-in addresses (never dereferenced)
+    _fill_valid_sizes(st)
+    n = len(mats)
+    assert _call_gemv(st, mats, [A] * n, [A] * n, A, 1 << 20) == rc
+
+
+def _fill_valid_sizes(st):
+    """Stand-in addresses and sizes consistent with the layout, so that the
+    stream descriptor itself passes the decoder's checks."""
+    T, B, n = int(st.layout.threads_per_block), int(st.sizes.num_blocks), int(st.sizes.n_elems)
+    st.exp = st.sm = st.gaps = st.tables = A
+    st.block_pos = A
+    st.sizes.max_code_len = 20
+    st.sizes.num_chunks = B * T
+    st.sizes.exp_bytes = B * 8 * T + 16
+    st.sizes.gap_bytes = 4 * ((5 * (B * T + 1) + 31) // 32 + 2)
+    st.sizes.sm_bytes = ((n + 15) & ~15) + 16
+    st.sizes.max_elems_per_block = 4096
+    st.sizes.table_bytes = codec.lib() and _table_bytes(int(st.layout.lut_bits))
+
+
+def _table_bytes(K):
+    cb = codec.codebook_from_counts(np.array([1, 1] + [0] * 254, np.uint64))
+    return codec.build_tables(cb, K).size
+
+
+def test_gemv_rejects_other_layouts_and_bad_buffers():
+    mats = [(0, 16, 2048)]
+    st = _stream_desc(T=256)
+    _fill_valid_sizes(st)
+    assert _call_gemv(st, mats, [A], [A], A, 1 << 20) == -6      # needs T = 64
+    st = _stream_desc()
+    _fill_valid_sizes(st)
+    assert _call_gemv(st, mats, [A + 8], [A], A, 1 << 20) == -1  # misaligned x
+    assert _call_gemv(st, mats, [A], [A + 2], A, 1 << 20) == -1  # misaligned y
+    assert _call_gemv(st, mats, [0], [A], A, 1 << 20) == -1      # null x
+    need = 4 * 8 * 4
+    assert _call_gemv(st, mats, [A], [A], A, need - 4) == -3     # short workspace
+    assert _call_gemv(st, mats, [A], [A], 0, need) == -1         # null workspace
+    out = ctypes.c_uint64()
+    assert codec.lib().df11_gemv_workspace_bytes(ctypes.byref(st), ctypes.byref(out)) == 0
+    assert out.value == need
