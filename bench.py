@@ -181,6 +181,7 @@ def cpu_model() -> str:
 
 
 DECODER_SOURCES = ("paper_2504_11651_amd/csrc/df11_decode.hip",
+                   "paper_2504_11651_amd/csrc/df11_decode_core.h",
                    "paper_2504_11651_amd/csrc/df11_tables.h")
 
 
