@@ -115,7 +115,7 @@ def run_stack(args) -> int:
     fused = None
     if T == 1:
         # fused decode-and-multiply (weights never written out), same step
-        gws = torch.empty(max(max(codec.gemv_workspace_bytes(d) for d in streams) // 4, 4),
+        gws = torch.empty(max(max(codec.gemv_workspace_bytes(d, mats) for d in streams) // 4, 4),
                           dtype=torch.float32, device=dev)
         xs1 = [x.reshape(-1) for x in xs]
         ys1 = [torch.empty(r, dtype=torch.float32, device=dev) for _, r, _ in mats]

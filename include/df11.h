@@ -229,12 +229,14 @@ int df11_block_forward(const df11_stream *dev, uint16_t *weights_out, const df11
  *              least 4096 weights;
  *   x:         host array of device pointers, x[m] = cols_m BF16, 16-byte aligned;
  *   y:         host array of device pointers, y[m] = rows_m fp32, 4-byte aligned;
- *   workspace: device, >= df11_gemv_workspace_bytes, 16-byte aligned.
+ *   workspace: device, >= df11_gemv_workspace_bytes (8 floats per stream
+ *              block plus 8 bytes per output row), 16-byte aligned.
  * The summation order is fixed by the stream's blocks (deterministic; it is
  * not the order df11_block_gemm uses, so results agree with it to rounding,
  * not bit for bit).  Enqueued on `stream`.  DF11_E_UNSUPPORTED for shapes or
  * layouts outside the requirements above. */
-int df11_gemv_workspace_bytes(const df11_stream *dev, uint64_t *bytes);
+int df11_gemv_workspace_bytes(const df11_stream *dev, const df11_matrix *mats, uint32_t n_mats,
+                              uint64_t *bytes);
 int df11_block_gemv(const df11_stream *dev, const df11_matrix *mats, uint32_t n_mats,
                     const uint16_t *const *x, float *const *y, void *workspace,
                     uint64_t workspace_bytes, hipStream_t stream);

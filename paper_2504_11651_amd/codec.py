@@ -118,7 +118,7 @@ def lib():
                             vp, u64, vp],
         "df11_block_forward": [P(Stream), vp, P(Matrix), ctypes.c_uint32, P(vp), ctypes.c_uint32,
                                P(vp), vp, u64, vp],
-        "df11_gemv_workspace_bytes": [P(Stream), P(u64)],
+        "df11_gemv_workspace_bytes": [P(Stream), P(Matrix), ctypes.c_uint32, P(u64)],
         "df11_block_gemv": [P(Stream), P(Matrix), ctypes.c_uint32, P(vp), P(vp), vp, u64, vp],
     }
     for name, args in sig.items():
@@ -366,10 +366,11 @@ def block_forward(ds: DeviceStream, weights_out, mats, xs, ys, workspace=None, s
 
 
 # ------------------------------------------------ fused decode-and-multiply
-def gemv_workspace_bytes(ds: DeviceStream) -> int:
-    """Workspace bytes block_gemv needs for this stream."""
+def gemv_workspace_bytes(ds: DeviceStream, mats) -> int:
+    """Workspace bytes block_gemv needs for this stream and these matrices."""
     out = ctypes.c_uint64()
-    _check(lib().df11_gemv_workspace_bytes(ctypes.byref(ds.struct()), ctypes.byref(out)),
+    _check(lib().df11_gemv_workspace_bytes(ctypes.byref(ds.struct()), _mats(mats), len(mats),
+                                           ctypes.byref(out)),
            "df11_gemv_workspace_bytes")
     return int(out.value)
 
@@ -387,7 +388,7 @@ def block_gemv(ds: DeviceStream, mats, xs, ys, workspace=None, stream=None):
         if y.numel() != rows or y.element_size() != 4 or not y.is_contiguous():
             raise ValueError("y[m] must be a contiguous fp32 tensor of rows elements")
     if workspace is None:
-        workspace = torch.empty(max(gemv_workspace_bytes(ds) // 4, 4), dtype=torch.float32,
+        workspace = torch.empty(max(gemv_workspace_bytes(ds, mats) // 4, 4), dtype=torch.float32,
                                 device=ds.device)
     xp = (ctypes.c_void_p * len(xs))(*[x.data_ptr() for x in xs])
     yp = (ctypes.c_void_p * len(ys))(*[y.data_ptr() for y in ys])

@@ -72,12 +72,17 @@ struct GemvArgs {
     uint32_t cols[kMaxM];
     Divider div[kMaxM];   // division by cols
     const uint16_t *x[kMaxM];
-    float *part;          // kSlots floats per block
+    uint32_t row_base[kMaxM];  // index of the matrix's first row among all rows
+    float *part;               // kSlots floats per block
+    uint32_t *first_block;     // per row: the block holding its first weight
+    uint32_t *last_block;      // per row: the block holding its last weight
 };
 
 struct ReduceArgs {
     const uint32_t *block_pos;  // B + 1 entries
     const float *part;
+    const uint32_t *first_block;
+    const uint32_t *last_block;
     uint32_t num_blocks;
     uint32_t n_mats;
     uint32_t row_start[kMaxM + 1];  // prefix sums of rows
@@ -196,6 +201,11 @@ __device__ __forceinline__ void dot_block(const GemvArgs &g, const Range &r, con
         if (lane == 63u)
             *reinterpret_cast<float4 *>(g.part + static_cast<uint64_t>(b) * kSlots + j * kSegSlots) =
                 make_float4(t0, t1, t2, 0.f);
+        if (lane < nrows) {  // rows whose first or last weight is in this block, one per lane
+            const uint64_t rs = uint64_t{off} + uint64_t{rlo + lane} * cols;
+            if (rs >= lo) g.first_block[g.row_base[m] + rlo + lane] = b;
+            if (rs + cols <= hi) g.last_block[g.row_base[m] + rlo + lane] = b;
+        }
     }
 }
 
@@ -271,19 +281,19 @@ __global__ __launch_bounds__(256) void df11_gemv_reduce_kernel(ReduceArgs ra) {
         }
     }
     const uint32_t row = i - rs;
-    const uint32_t start = off + row * cols, stop = start + cols;
-    // last block whose first weight is <= start (the non-empty block holding it)
-    uint32_t lo = 0, hi = ra.num_blocks;  // invariant: block_pos[lo] <= start < block_pos[hi]
-    while (hi - lo > 1u) {
-        const uint32_t mid = (lo + hi) >> 1;
-        if (ra.block_pos[mid] <= start) lo = mid;
-        else hi = mid;
+    // every block between the row's first and last holds at least one weight
+    // (each 64-bit chunk starts a code), so all of them wrote partial sums
+    const uint32_t fb = ra.first_block[i], lb = ra.last_block[i];
+    // a block holds >= 128 weights (64 chunks, >= 2 codes each), so a row
+    // spans at most cols / 128 + 2 blocks; indices outside that (not written
+    // by the decode kernel) give NaN instead of reads out of range
+    if (lb >= ra.num_blocks || fb > lb || lb - fb > cols / 128u + 2u) {
+        y[row] = __builtin_nanf("");
+        return;
     }
     float sum = 0.f;
-    for (uint32_t b = lo; b < ra.num_blocks; ++b) {
-        const uint32_t bs = ra.block_pos[b], be = ra.block_pos[b + 1];
-        if (bs >= stop) break;
-        if (be <= bs) continue;  // empty block
+    for (uint32_t b = fb; b <= lb; ++b) {
+        const uint32_t bs = ra.block_pos[b];
         const uint32_t j = off <= bs ? 0u : 1u;
         const uint32_t seg_lo = bs > off ? bs : off;
         const uint32_t rlo = (seg_lo - off) / cols;
@@ -344,6 +354,13 @@ int gemv_shape(uint32_t lut_bits, uint32_t buf, uint32_t *W_out, uint32_t *grid_
     return DF11_OK;
 }
 
+// partial sums (kSlots floats per block), then first and last block per row
+uint64_t workspace_bytes_for(const df11_stream *s, const df11_matrix *mats, uint32_t n_mats) {
+    uint64_t rows = 0;
+    for (uint32_t m = 0; m < n_mats; ++m) rows += mats[m].rows;
+    return 4ull * kSlots * s->sizes.num_blocks + 8ull * rows;
+}
+
 int check_gemv(const df11_stream *s, const df11_matrix *mats, uint32_t n_mats) {
     int rc = check_stream(s);
     if (rc) return rc;
@@ -368,9 +385,10 @@ int check_gemv(const df11_stream *s, const df11_matrix *mats, uint32_t n_mats) {
 
 extern "C" {
 
-int df11_gemv_workspace_bytes(const df11_stream *dev, uint64_t *bytes) {
-    if (!dev || !bytes) return DF11_E_INVALID_ARG;
-    *bytes = 4ull * kSlots * dev->sizes.num_blocks;
+int df11_gemv_workspace_bytes(const df11_stream *dev, const df11_matrix *mats, uint32_t n_mats,
+                              uint64_t *bytes) {
+    if (!dev || !bytes || !mats || n_mats == 0 || n_mats > kMaxM) return DF11_E_INVALID_ARG;
+    *bytes = workspace_bytes_for(dev, mats, n_mats);
     return DF11_OK;
 }
 
@@ -384,7 +402,7 @@ int df11_block_gemv(const df11_stream *dev, const df11_matrix *mats, uint32_t n_
         if (!x[m] || !y[m] || (reinterpret_cast<uintptr_t>(x[m]) & 15u) ||
             (reinterpret_cast<uintptr_t>(y[m]) & 3u))
             return DF11_E_INVALID_ARG;
-    const uint64_t need = 4ull * kSlots * dev->sizes.num_blocks;
+    const uint64_t need = workspace_bytes_for(dev, mats, n_mats);
     if (workspace_bytes < need) return DF11_E_BUFFER_TOO_SMALL;
     if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 15u)) return DF11_E_INVALID_ARG;
     if (dev->sizes.n_elems == 0) return DF11_OK;
@@ -430,10 +448,17 @@ int df11_block_gemv(const df11_stream *dev, const df11_matrix *mats, uint32_t n_
         }
         g.x[m] = x[m];
         ra.y[m] = y[m];
-        ra.row_start[m] = static_cast<uint32_t>(rows);
+        ra.row_start[m] = g.row_base[m] = static_cast<uint32_t>(rows);
         rows += mats[m].rows;
     }
     for (uint32_t m = n_mats; m <= kMaxM; ++m) ra.row_start[m] = static_cast<uint32_t>(rows);
+    if (rows > 0xFFFFFFFFull) return DF11_E_UNSUPPORTED;
+    uint32_t *row_blocks = reinterpret_cast<uint32_t *>(static_cast<uint8_t *>(workspace) +
+                                                        4ull * kSlots * a.num_blocks);
+    g.first_block = row_blocks;
+    g.last_block = row_blocks + rows;
+    ra.first_block = g.first_block;
+    ra.last_block = g.last_block;
 
     uint32_t W = 0, grid_max = 0;
     rc = gemv_shape(a.lut_bits, a.buf_bytes, &W, &grid_max);

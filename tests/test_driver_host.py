@@ -163,9 +163,10 @@ def test_gemv_rejects_other_layouts_and_bad_buffers():
     assert _call_gemv(st, mats, [A + 8], [A], A, 1 << 20) == -1  # misaligned x
     assert _call_gemv(st, mats, [A], [A + 2], A, 1 << 20) == -1  # misaligned y
     assert _call_gemv(st, mats, [0], [A], A, 1 << 20) == -1      # null x
-    need = 4 * 8 * 4
+    need = 4 * 8 * 4 + 8 * 16  # 8 floats per block (4 blocks), two indices per row (16 rows)
     assert _call_gemv(st, mats, [A], [A], A, need - 4) == -3     # short workspace
     assert _call_gemv(st, mats, [A], [A], 0, need) == -1         # null workspace
     out = ctypes.c_uint64()
-    assert codec.lib().df11_gemv_workspace_bytes(ctypes.byref(st), ctypes.byref(out)) == 0
+    assert codec.lib().df11_gemv_workspace_bytes(ctypes.byref(st), codec._mats(mats), 1,
+                                                 ctypes.byref(out)) == 0
     assert out.value == need
