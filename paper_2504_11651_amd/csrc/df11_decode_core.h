@@ -361,6 +361,19 @@ __device__ __forceinline__ void assemble_block(const DecodeArgs &a, const Range 
                     assemble_group(buf, g, *reinterpret_cast<const uint2 *>(a.sm + r.g0 + (g << 3))));
 }
 
+// Workgroups are dispatched to the 8 XCDs round robin and each XCD has its
+// own L2.  Within every run of 32 workgroups this numbering gives the 4 that
+// share an XCD neighbouring indices, so neighbouring blocks, which share the
+// cache lines at their boundaries, are mostly decoded under one L2, while
+// the blocks in flight still form one contiguous window of the stream.  A
+// bijection of [0, n): a trailing partial run keeps its own numbers.
+__device__ __forceinline__ uint32_t xcd_grouped_index(uint32_t g, uint32_t n) {
+    constexpr uint32_t kXcds = 8u, kPer = 4u, kRun = kXcds * kPer;
+    const uint32_t base = g - g % kRun;
+    if (base + kRun > n) return g;
+    return base + (g % kXcds) * kPer + (g % kRun) / kXcds;
+}
+
 __device__ __forceinline__ void stage_table_blob(const DecodeArgs &a, uint8_t *lds, uint32_t tid,
                                                  uint32_t nthreads) {
     const uint4 *src = reinterpret_cast<const uint4 *>(a.tables);

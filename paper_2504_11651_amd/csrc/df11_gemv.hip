@@ -225,7 +225,7 @@ __global__ __launch_bounds__(64 * W) void df11_gemv_wave_kernel(GemvArgs g) {
     const uint32_t cap = a.buf_bytes - 8u;
     __syncthreads();
 
-    const uint32_t first_block = blockIdx.x * W + wave;
+    const uint32_t first_block = xcd_grouped_index(blockIdx.x, gridDim.x) * W + wave;
     const uint32_t stride = gridDim.x * W;
     if (first_block >= a.num_blocks) return;
     ChunkWords cw = load_chunk(a, first_block, first_block * 64u + lane);
