@@ -15,8 +15,11 @@
 //      table until the code start reaches the next chunk's first code;
 //   3. exclusive scan of the counts (wave DPP scan, plus LDS across waves
 //      for T >= 128) gives each lane its output position (Sec. 2.3.2);
-//   4. phase 2 (emit): decode again and OR the exponent bytes into an LDS
-//      buffer at their output positions.  A lookup may run past the lane's
+//   4. phase 2 (emit): replay the lookups phase 1 kept in registers (a
+//      chunk that needed more decodes its remaining codes again) and OR the
+//      exponent bytes into an LDS buffer at their output positions.  The
+//      waves of a CU run this phase at a higher priority than decoding, and
+//      step 5 higher still.  A lookup may run past the lane's
 //      last code; the extra codes are the next lanes' first codes, decoded
 //      from the same bits, so they land on their own positions with their
 //      own values and need no masking;
