@@ -274,7 +274,9 @@ __device__ __forceinline__ Range block_range(const DecodeArgs &a, const ChunkWor
     Range r;
     r.s = umin(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(cw.bp0)), a.n_elems);
     uint32_t e = umax(umin(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(cw.bp1)), a.n_elems), r.s);
-    e = umin(e, r.s + (a.buf_bytes - kBufSlack));
+    // at most the buffer's worth; the room above r.s is clamped so the sum
+    // cannot wrap for a stream ending near 2^32 weights
+    e = umin(e, r.s + umin(a.buf_bytes - kBufSlack, 0xFFFFFFFFu - r.s));
     r.shift = r.s & 7u;
     r.lim = r.shift + (e - r.s);
     r.g0 = r.s - r.shift;

@@ -164,12 +164,12 @@ __device__ __forceinline__ void dot_block(const GemvArgs &g, const Range &r, con
         float acc[3] = {0.f, 0.f, 0.f};
         auto group = [&](uint32_t gi, uint2 Sg, auto one_row) {
             const uint32_t E = r.g0 + (gi << 3);
-            if (E + 8u <= lo || E >= hi) return;
+            if ((E < lo && lo - E >= 8u) || E >= hi) return;  // (no E + 8: it may wrap)
             const uint32_t row = one_row ? rlo : rlo + (E >= b1 ? 1u : 0u) + (E >= b2 ? 1u : 0u);
             const uint32_t kcol = E - off - row * cols;
             uint4 w = assemble_group(buf, gi, Sg);
             uint4 xv = *reinterpret_cast<const uint4 *>(x + kcol);
-            if (E < lo || E + 8u > hi) {  // a group shared with a neighbour: its elements only
+            if (E < lo || hi - E < 8u) {  // a group shared with a neighbour: its elements only
                 const uint4 mk = element_mask(lo > E ? lo - E : 0u, umin(hi - E, 8u));
                 w = make_uint4(w.x & mk.x, w.y & mk.y, w.z & mk.z, w.w & mk.w);
                 xv = make_uint4(xv.x & mk.x, xv.y & mk.y, xv.z & mk.z, xv.w & mk.w);
