@@ -6,7 +6,7 @@ resident in HBM, into a reused BF16 workspace -- the whole decode path in
 one launch.  Prints one JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                  [--tokens T] [--no-cpu-baseline] [--calib] [--cold]
+                  [--tokens T] [--no-cpu-baseline] [--calib] [--no-cold]
 
 --workload llama3_8b_stack times the decode-then-products driver instead: 32
 blocks resident in compressed form, one step = decode one block into a reused
@@ -248,8 +248,9 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib", action="store_true",
                     help="also run a plain device copy of known size (PMC calibration)")
-    ap.add_argument("--cold", action="store_true",
-                    help="also time steps with the 256 MB last-level cache flushed before each")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the extra cold-cache launches (each after a 1 GiB read that "
+                         "evicts the 256 MB last-level cache and the L2)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -315,10 +316,10 @@ def main() -> int:
     ev_ms = np.array([s_ev.elapsed_time(e_ev) for s_ev, e_ev in per])
 
     cold = None
-    if args.cold:
+    if not args.no_cold:
         scratch = torch.ones(1 << 28, dtype=torch.int32, device=dev)  # 1 GiB
         cms = []
-        for i in range(max(5, min(args.steps // 5, 50))):
+        for i in range(max(5, min(args.steps // 5, 20))):
             scratch.sum()  # evicts the MALL and L2 by reading 1 GiB (no dirty lines left)
             s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             s.record(stream)
