@@ -62,7 +62,7 @@ def run_stack(args) -> int:
     blocks = 32
     mats, n = stack_mats()
     t0 = time.perf_counter()
-    streams, comp_bytes, w0 = [], [], None
+    streams, comp_bytes, w0, hs0 = [], [], None, None
     for i in range(blocks):
         w, _ = synth.llama3_8b_stack_block(i)
         hs = codec.encode(w)
@@ -71,11 +71,13 @@ def run_stack(args) -> int:
                           int(z.block_pos_bytes) + int(z.table_bytes))
         streams.append(codec.to_device(hs, dev))
         if i == 0:
-            w0 = w
+            w0, hs0 = w, hs
     t_prep = time.perf_counter() - t0
     T = args.tokens
-    x1 = torch.from_numpy(synth.activations(T, 4096, 5, 0, 1).view(np.int16)).to(dev)
-    x2 = torch.from_numpy(synth.activations(T, 14336, 5, 0, 2).view(np.int16)).to(dev)
+    x1_h = synth.activations(T, 4096, 5, 0, 1)
+    x2_h = synth.activations(T, 14336, 5, 0, 2)
+    x1 = torch.from_numpy(x1_h.view(np.int16)).to(dev)
+    x2 = torch.from_numpy(x2_h.view(np.int16)).to(dev)
     xs = [x1.view(torch.bfloat16)] * 6 + [x2.view(torch.bfloat16)]
     ys = [torch.empty((T, r), dtype=torch.float32, device=dev) for _, r, _ in mats]
     ws = torch.empty(max(codec.gemm_workspace_bytes(mats, T) // 4, 1), dtype=torch.float32,
@@ -160,14 +162,43 @@ def run_stack(args) -> int:
         "kernel_ms": {"step_in_timed_region": round(step_ms, 5), "decode": round(dec_ms, 5),
                       "products": round(gemm_ms, 5)},
         "products_gbs": round(gemm_bytes / (gemm_ms * 1e-3) / 1e9, 1),
+        "products_roofline": {"bound": "hbm", "achieved": round(gemm_bytes / (gemm_ms * 1e-3) / 1e9, 1),
+                              "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                              "frac": round(gemm_bytes / (gemm_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                              "traffic": None},
         "tokens_per_s_per_block": round(T / (wall_ms * 1e-3), 1),
         "compressed_bytes_resident": int(sum(comp_bytes)),
         "host_s": {"generate_and_encode": round(t_prep, 2)},
     }
     if fused is not None:
         rec["fused_decode_gemv"] = fused
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = stack_cpu_baseline(hs0, w0, mats, [x1_h] * 6 + [x2_h], n)
     print(json.dumps(rec), flush=True)
     return 0
+
+
+def stack_cpu_baseline(hs, w, mats, xs, n) -> dict:
+    """One block step by the oracle on one host thread: bit-serial decode of
+    the block's stream, then its 7 products in float64."""
+    import oracle
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        dec = oracle.decode_serial(hs.exp, int(hs.sizes.total_bits), hs.sm, n,
+                                   hs.codebook.lengths)
+        t_dec = time.perf_counter() - t0
+        assert np.array_equal(dec, w), "oracle decode differs from the input"
+        t0 = time.perf_counter()
+        for (off, r, c), x in zip(mats, xs):
+            oracle.linear(x, dec[off:off + r * c].reshape(r, c))
+        t_mm = time.perf_counter() - t0
+    t = t_dec + t_mm
+    return {"value": round(2.0 * n / t / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"block 0 of the stack: bit-serial decode ({t_dec:.1f} s) and the 7 "
+                      f"products in float64 ({t_mm:.1f} s), 1 thread of {os.cpu_count()} on "
+                      f"{cpu_model()}",
+            "ms_per_step": round(t * 1e3, 1)}
 
 
 def cpu_model() -> str:
