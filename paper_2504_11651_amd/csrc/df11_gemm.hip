@@ -13,7 +13,8 @@
 //     issues v_mfma_f32_16x16x32_bf16 twice per 16-token slice; A (tokens)
 //     and B (features) use the same assignment of k to lanes, so the dot
 //     products cover each k once whatever order the unit sums in;
-//   - a matrix wider than 4096 columns is split into k ranges; each range
+//   - a matrix is split into k ranges of about 1024 columns (up to 32
+//     tokens) or 4096 columns (more tokens); each range of a split matrix
 //     writes fp32 partial sums, and a second kernel adds them in a fixed
 //     order, so results are deterministic (no atomics).
 #include <hip/hip_runtime.h>
@@ -31,7 +32,13 @@ constexpr uint32_t kTileRows = 16;   // output features per wave
 constexpr uint32_t kKStep = 64;      // k per inner step: two MFMAs
 constexpr uint32_t kUnroll = 4;      // inner steps whose weight loads are issued together
 constexpr uint32_t kKPerIter = kKStep * kUnroll;
-constexpr uint32_t kKTarget = 4096;  // k range of one wave before a matrix is split
+// k range of one wave before a matrix is split: short ranges (more
+// workgroups in flight) pay off while the products are light; from 33
+// tokens the products per weight favour long ranges
+constexpr uint32_t kKTargetFew = 1024;
+constexpr uint32_t kKTargetMany = 4096;
+constexpr uint32_t kFewTokens = 32;
+constexpr uint32_t kSlabMinTokens = 4;  // fewer tokens: activations straight from memory
 constexpr uint32_t kWaves = 4;       // waves per workgroup
 constexpr uint32_t kMax = DF11_MAX_MATRICES;
 
@@ -135,8 +142,8 @@ __device__ __forceinline__ void write_tile(const GemmArgs &a, const Mat &m, uint
 // half h gives lane group g the 8 values kk + 32h + 8g .. +7, so the four
 // lanes of one row read 64 contiguous bytes per load.
 
-// Up to 16 tokens: one wavefront per 16-feature tile, activations read
-// straight from memory (a few KiB, cache resident).
+// Up to 3 tokens: one wavefront per 16-feature tile, activations read
+// straight from memory (a few hundred bytes per k range, cache resident).
 __global__ __launch_bounds__(64 * kWaves) void gemm_tiles_kernel(GemmArgs a) {
     const uint32_t lane = threadIdx.x & 63u;
     const uint32_t tile =
@@ -180,7 +187,7 @@ __global__ __launch_bounds__(64 * kWaves) void gemm_tiles_kernel(GemmArgs a) {
     write_tile<1>(a, m, rb, s, j, g, acc);
 }
 
-// More than 16 tokens: a workgroup of kWaves waves covers 16*kWaves features
+// Four or more tokens: a workgroup of kWaves waves covers 16*kWaves features
 // over one k range and stages the activations of each 256-k slab in LDS once
 // for all its waves (rows padded by 16 bytes so the 16 lanes of one read
 // pass hit distinct banks).  Weights still stream straight into registers.
@@ -316,10 +323,11 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(ReduceArgs a) {
     y[static_cast<uint64_t>(t) * rows + f] = sum;
 }
 
-// Work split of one matrix: k ranges of at most about kKTarget, each a
+// Work split of one matrix: k ranges of at most about the k target, each a
 // multiple of kKPerIter except the last.
-void split_of(uint32_t cols, uint32_t *ksplit, uint32_t *kchunk) {
-    uint32_t ks = (cols + kKTarget - 1) / kKTarget;
+void split_of(uint32_t cols, uint32_t tokens, uint32_t *ksplit, uint32_t *kchunk) {
+    const uint32_t target = tokens <= kFewTokens ? kKTargetFew : kKTargetMany;
+    uint32_t ks = (cols + target - 1) / target;
     if (ks == 0) ks = 1;
     uint32_t kc = (cols + ks - 1) / ks;
     kc = (kc + kKPerIter - 1) / kKPerIter * kKPerIter;
@@ -343,7 +351,7 @@ uint64_t workspace_floats(const df11_matrix *mats, uint32_t n_mats, uint32_t tok
     uint64_t f = 0;
     for (uint32_t m = 0; m < n_mats; ++m) {
         uint32_t ks, kc;
-        split_of(mats[m].cols, &ks, &kc);
+        split_of(mats[m].cols, tokens, &ks, &kc);
         if (ks > 1) f += static_cast<uint64_t>(mats[m].rows) * ks * tokens;
     }
     return f;
@@ -378,7 +386,7 @@ int plan(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats, u
             (reinterpret_cast<uintptr_t>(y[m]) & 3u))
             return DF11_E_INVALID_ARG;
         uint32_t ks, kc;
-        split_of(d.cols, &ks, &kc);
+        split_of(d.cols, tokens, &ks, &kc);
         g.tile_start[m] = static_cast<uint32_t>(tiles);
         g.wg_start[m] = static_cast<uint32_t>(wgs);
         g.ksplit[m] = r.ksplit[m] = ks;
@@ -416,7 +424,12 @@ int launch(const GemmArgs &g, const ReduceArgs &r, hipStream_t stream) {
     const dim3 block(64 * kWaves);
     const dim3 grid_tiles((g.num_tiles + kWaves - 1) / kWaves), grid_wg(g.num_wg);
     switch (mt) {
-    case 1: hipLaunchKernelGGL(gemm_tiles_kernel, grid_tiles, block, 0, stream, g); break;
+    case 1:
+        if (g.tokens < kSlabMinTokens)
+            hipLaunchKernelGGL(gemm_tiles_kernel, grid_tiles, block, 0, stream, g);
+        else
+            hipLaunchKernelGGL(gemm_slab_kernel<1>, grid_wg, block, 0, stream, g);
+        break;
     case 2: hipLaunchKernelGGL(gemm_slab_kernel<2>, grid_wg, block, 0, stream, g); break;
     case 3: hipLaunchKernelGGL(gemm_slab_kernel<3>, grid_wg, block, 0, stream, g); break;
     default: hipLaunchKernelGGL(gemm_slab_kernel<4>, grid_wg, block, 0, stream, g); break;

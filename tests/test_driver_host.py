@@ -22,15 +22,24 @@ def llama_mats():
 
 
 def test_workspace_closed_form():
-    # only down (14336 columns) is split: 4 k-ranges of 3584; partial sums of
-    # 4096 rows x 4 ranges x tokens floats
+    # up to 32 tokens every matrix is split into k ranges of 1024 columns
+    # (4 for the 4096-column matrices, 14 for down); partial sums of rows x
+    # ranges x tokens floats
     mats, _ = llama_mats()
-    for t in (1, 7, 16, 64):
+    few = 4 * (4096 + 1024 + 1024 + 4096 + 14336 + 14336) + 14 * 4096
+    for t in (1, 7, 16, 32):
+        assert codec.gemm_workspace_bytes(mats, t) == 4 * few * t
+    # from 33 tokens only down (14336 columns) is split: 4 ranges of 3584
+    for t in (33, 64):
         assert codec.gemm_workspace_bytes(mats, t) == 4 * 4096 * 4 * t
-    assert codec.gemm_workspace_bytes([(0, 16, 4096)], 5) == 0
-    # 8192 columns -> 2 ranges; 28672 -> 7 ranges
-    assert codec.gemm_workspace_bytes([(0, 32, 8192)], 3) == 4 * 32 * 2 * 3
-    assert codec.gemm_workspace_bytes([(0, 32, 28672)], 2) == 4 * 32 * 7 * 2
+    assert codec.gemm_workspace_bytes([(0, 16, 1024)], 5) == 0
+    assert codec.gemm_workspace_bytes([(0, 16, 4096)], 40) == 0
+    assert codec.gemm_workspace_bytes([(0, 16, 4096)], 5) == 4 * 16 * 4 * 5
+    # 8192 columns -> 8 ranges (few tokens) or 2; 28672 -> 28 or 7
+    assert codec.gemm_workspace_bytes([(0, 32, 8192)], 3) == 4 * 32 * 8 * 3
+    assert codec.gemm_workspace_bytes([(0, 32, 8192)], 40) == 4 * 32 * 2 * 40
+    assert codec.gemm_workspace_bytes([(0, 32, 28672)], 2) == 4 * 32 * 28 * 2
+    assert codec.gemm_workspace_bytes([(0, 32, 28672)], 64) == 4 * 32 * 7 * 64
 
 
 @pytest.mark.parametrize("mats,tokens,rc", [
