@@ -14,12 +14,15 @@
 //     and B (features) use the same assignment of k to lanes, so the dot
 //     products cover each k once whatever order the unit sums in;
 //   - a matrix is split into k ranges of about 1024 columns (up to 32
-//     tokens) or 4096 columns (more tokens); each range of a split matrix
-//     writes fp32 partial sums, and a second kernel adds them in a fixed
-//     order, so results are deterministic (no atomics).
+//     tokens) or 4096 columns, or half that where it evens out the work per
+//     CU (more tokens); each range of a split matrix writes fp32 partial
+//     sums, and a second kernel adds them in a fixed order, so results are
+//     deterministic (no atomics).
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <mutex>
+#include <vector>
 
 #include "df11.h"
 
@@ -34,7 +37,8 @@ constexpr uint32_t kUnroll = 4;      // inner steps whose weight loads are issue
 constexpr uint32_t kKPerIter = kKStep * kUnroll;
 // k range of one wave before a matrix is split: short ranges (more
 // workgroups in flight) pay off while the products are light; from 33
-// tokens the products per weight favour long ranges
+// tokens the products per weight favour long ranges, and the split is
+// chosen to balance the CUs
 constexpr uint32_t kKTargetFew = 1024;
 constexpr uint32_t kKTargetMany = 4096;
 constexpr uint32_t kFewTokens = 32;
@@ -323,17 +327,111 @@ __global__ __launch_bounds__(256) void gemm_reduce_kernel(ReduceArgs a) {
     y[static_cast<uint64_t>(t) * rows + f] = sum;
 }
 
-// Work split of one matrix: k ranges of at most about the k target, each a
-// multiple of kKPerIter except the last.
-void split_of(uint32_t cols, uint32_t tokens, uint32_t *ksplit, uint32_t *kchunk) {
-    const uint32_t target = tokens <= kFewTokens ? kKTargetFew : kKTargetMany;
-    uint32_t ks = (cols + target - 1) / target;
-    if (ks == 0) ks = 1;
-    uint32_t kc = (cols + ks - 1) / ks;
+// Split of one matrix into about ks_req k ranges, each a whole number of
+// slabs (kKPerIter) except the last.
+void split_into(uint32_t cols, uint32_t ks_req, uint32_t *ksplit, uint32_t *kchunk) {
+    uint32_t kc = (cols + ks_req - 1) / ks_req;
     kc = (kc + kKPerIter - 1) / kKPerIter * kKPerIter;
-    ks = (cols + kc - 1) / kc;  // no empty range
-    *ksplit = ks;
     *kchunk = kc;
+    *ksplit = (cols + kc - 1) / kc;  // no empty range
+}
+
+uint32_t base_ranges(uint32_t cols, uint32_t tokens) {
+    const uint32_t target = tokens <= kFewTokens ? kKTargetFew : kKTargetMany;
+    const uint32_t ks = (cols + target - 1) / target;
+    return ks ? ks : 1u;
+}
+
+// Estimated bytes moved by the busiest CU for one choice of k ranges per
+// matrix: workgroup i runs on CU i mod cus (with many tokens every
+// workgroup of the launch is resident at once), moving its weights and,
+// for a split matrix, writing its partial sums; the reduce kernel's traffic
+// is spread over all CUs.
+uint64_t split_cost(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens, uint32_t cus,
+                    const uint32_t *ks_req, std::vector<uint64_t> &load) {
+    load.assign(cus, 0);
+    uint64_t wg = 0, reduce = 0;
+    for (uint32_t m = 0; m < n_mats; ++m) {
+        uint32_t ks, kc;
+        split_into(mats[m].cols, ks_req[m], &ks, &kc);
+        const uint32_t rows = mats[m].rows, cols = mats[m].cols;
+        for (uint32_t r0 = 0; r0 < rows; r0 += kTileRows * kWaves) {
+            const uint64_t nr = rows - r0 < kTileRows * kWaves ? rows - r0 : kTileRows * kWaves;
+            for (uint32_t s = 0; s < ks; ++s) {
+                const uint64_t len = cols - s * kc < kc ? cols - s * kc : kc;
+                load[wg++ % cus] += 2 * nr * len + (ks > 1 ? 4 * nr * tokens : 0);
+            }
+        }
+        if (ks > 1) reduce += 4ull * rows * tokens * (ks + 1);
+    }
+    uint64_t most = 0;
+    for (uint64_t l : load) most = l > most ? l : most;
+    return most + reduce / cus;
+}
+
+// With many tokens the products per weight are heavy enough that the CU
+// holding the most work sets the time: of the choices of 1x or 2x the base
+// number of k ranges per matrix, take the one whose busiest CU moves the
+// fewest bytes (ties: fewer workgroups).  Cached per device and shapes.
+struct SplitEntry {
+    int dev;
+    uint32_t tokens, n_mats, rows[kMax], cols[kMax], ks_req[kMax];
+};
+std::mutex g_split_mu;
+std::vector<SplitEntry> g_splits;
+constexpr size_t kMaxSplits = 64;
+
+int choose_ranges(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens, uint32_t *ks_req) {
+    for (uint32_t m = 0; m < n_mats; ++m) ks_req[m] = base_ranges(mats[m].cols, tokens);
+    if (tokens <= kFewTokens) return DF11_OK;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return DF11_E_HIP;
+    std::lock_guard<std::mutex> lk(g_split_mu);
+    for (const SplitEntry &e : g_splits) {
+        bool same = e.dev == dev && e.tokens == tokens && e.n_mats == n_mats;
+        for (uint32_t m = 0; same && m < n_mats; ++m)
+            same = e.rows[m] == mats[m].rows && e.cols[m] == mats[m].cols;
+        if (same) {
+            for (uint32_t m = 0; m < n_mats; ++m) ks_req[m] = e.ks_req[m];
+            return DF11_OK;
+        }
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+        return DF11_E_HIP;
+    uint32_t base[kMax], trial[kMax], best_mask = 0;
+    for (uint32_t m = 0; m < n_mats; ++m) base[m] = ks_req[m];
+    std::vector<uint64_t> load;
+    uint64_t best = ~0ull, best_wg = ~0ull;
+    for (uint32_t mask = 0; mask < (1u << n_mats); ++mask) {
+        uint64_t wg = 0;
+        for (uint32_t m = 0; m < n_mats; ++m) {
+            trial[m] = base[m] << ((mask >> m) & 1u);
+            uint32_t ks, kc;
+            split_into(mats[m].cols, trial[m], &ks, &kc);
+            wg += uint64_t{(mats[m].rows + kTileRows * kWaves - 1) / (kTileRows * kWaves)} * ks;
+        }
+        const uint64_t c = split_cost(mats, n_mats, tokens, static_cast<uint32_t>(cus), trial, load);
+        if (c < best || (c == best && wg < best_wg)) {
+            best = c;
+            best_wg = wg;
+            best_mask = mask;
+        }
+    }
+    SplitEntry e{};
+    e.dev = dev;
+    e.tokens = tokens;
+    e.n_mats = n_mats;
+    for (uint32_t m = 0; m < n_mats; ++m) {
+        ks_req[m] = base[m] << ((best_mask >> m) & 1u);
+        e.rows[m] = mats[m].rows;
+        e.cols[m] = mats[m].cols;
+        e.ks_req[m] = ks_req[m];
+    }
+    if (g_splits.size() >= kMaxSplits) g_splits.clear();  // bounded lookup cost
+    g_splits.push_back(e);
+    return DF11_OK;
 }
 
 int check_mats(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens) {
@@ -347,11 +445,14 @@ int check_mats(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens) {
     return DF11_OK;
 }
 
+// Partial-sum floats any device's choice of k ranges needs (with many
+// tokens, the most the choice between 1x and 2x the base ranges can take).
 uint64_t workspace_floats(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens) {
     uint64_t f = 0;
     for (uint32_t m = 0; m < n_mats; ++m) {
         uint32_t ks, kc;
-        split_of(mats[m].cols, tokens, &ks, &kc);
+        const uint32_t base = base_ranges(mats[m].cols, tokens);
+        split_into(mats[m].cols, tokens <= kFewTokens ? base : 2 * base, &ks, &kc);
         if (ks > 1) f += static_cast<uint64_t>(mats[m].rows) * ks * tokens;
     }
     return f;
@@ -370,6 +471,18 @@ int plan(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats, u
     if (need && (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 15u)))
         return DF11_E_INVALID_ARG;
 
+    for (uint32_t m = 0; m < n_mats; ++m) {
+        const df11_matrix &d = mats[m];
+        if (d.offset > n_weights || static_cast<uint64_t>(d.rows) * d.cols > n_weights - d.offset)
+            return DF11_E_INVALID_ARG;
+        if (!x[m] || !y[m] || (reinterpret_cast<uintptr_t>(x[m]) & 15u) ||
+            (reinterpret_cast<uintptr_t>(y[m]) & 3u))
+            return DF11_E_INVALID_ARG;
+    }
+    uint32_t ks_req[kMax];
+    rc = choose_ranges(mats, n_mats, tokens, ks_req);
+    if (rc) return rc;
+
     GemmArgs g{};
     ReduceArgs r{};
     g.w = weights;
@@ -380,13 +493,8 @@ int plan(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats, u
     uint64_t tiles = 0, wgs = 0, part = 0, outs = 0;
     for (uint32_t m = 0; m < n_mats; ++m) {
         const df11_matrix &d = mats[m];
-        if (d.offset > n_weights || static_cast<uint64_t>(d.rows) * d.cols > n_weights - d.offset)
-            return DF11_E_INVALID_ARG;
-        if (!x[m] || !y[m] || (reinterpret_cast<uintptr_t>(x[m]) & 15u) ||
-            (reinterpret_cast<uintptr_t>(y[m]) & 3u))
-            return DF11_E_INVALID_ARG;
         uint32_t ks, kc;
-        split_of(d.cols, tokens, &ks, &kc);
+        split_into(d.cols, ks_req[m], &ks, &kc);
         g.tile_start[m] = static_cast<uint32_t>(tiles);
         g.wg_start[m] = static_cast<uint32_t>(wgs);
         g.ksplit[m] = r.ksplit[m] = ks;

@@ -29,17 +29,21 @@ def test_workspace_closed_form():
     few = 4 * (4096 + 1024 + 1024 + 4096 + 14336 + 14336) + 14 * 4096
     for t in (1, 7, 16, 32):
         assert codec.gemm_workspace_bytes(mats, t) == 4 * few * t
-    # from 33 tokens only down (14336 columns) is split: 4 ranges of 3584
+    # from 33 tokens the base ranges are 4096 columns (1 per 4096-column
+    # matrix, 4 for down) and a device may double any matrix's ranges to
+    # balance its CUs: the workspace covers the doubled split of every matrix
+    many = 2 * (4096 + 1024 + 1024 + 4096 + 14336 + 14336) + 8 * 4096
     for t in (33, 64):
-        assert codec.gemm_workspace_bytes(mats, t) == 4 * 4096 * 4 * t
+        assert codec.gemm_workspace_bytes(mats, t) == 4 * many * t
     assert codec.gemm_workspace_bytes([(0, 16, 1024)], 5) == 0
-    assert codec.gemm_workspace_bytes([(0, 16, 4096)], 40) == 0
+    assert codec.gemm_workspace_bytes([(0, 16, 256)], 40) == 0
+    assert codec.gemm_workspace_bytes([(0, 16, 4096)], 40) == 4 * 16 * 2 * 40
     assert codec.gemm_workspace_bytes([(0, 16, 4096)], 5) == 4 * 16 * 4 * 5
-    # 8192 columns -> 8 ranges (few tokens) or 2; 28672 -> 28 or 7
+    # 8192 columns -> 8 ranges (few tokens) or up to 4; 28672 -> 28 or up to 14
     assert codec.gemm_workspace_bytes([(0, 32, 8192)], 3) == 4 * 32 * 8 * 3
-    assert codec.gemm_workspace_bytes([(0, 32, 8192)], 40) == 4 * 32 * 2 * 40
+    assert codec.gemm_workspace_bytes([(0, 32, 8192)], 40) == 4 * 32 * 4 * 40
     assert codec.gemm_workspace_bytes([(0, 32, 28672)], 2) == 4 * 32 * 28 * 2
-    assert codec.gemm_workspace_bytes([(0, 32, 28672)], 64) == 4 * 32 * 7 * 64
+    assert codec.gemm_workspace_bytes([(0, 32, 28672)], 64) == 4 * 32 * 14 * 64
 
 
 @pytest.mark.parametrize("mats,tokens,rc", [
@@ -79,6 +83,11 @@ def test_argument_rejections():
     assert _call_gemm(A, 1024, mats, [A + 8], [A], 1, 0, 0) == -1       # misaligned x
     assert _call_gemm(A, 1024, mats, [A], [A + 2], 1, 0, 0) == -1       # misaligned y
     assert _call_gemm(A, 1024, mats, [0], [A], 1, 0, 0) == -1           # null x
+    # with many tokens too (the per-device choice of k ranges comes after
+    # every argument check)
+    assert _call_gemm(A, 1023, mats, [A], [A], 64, 0, 0) == -1          # matrix past the block
+    assert _call_gemm(A, 1024, mats, [A + 8], [A], 64, 0, 0) == -1      # misaligned x
+    assert _call_gemm(A, 1024, mats, [A], [0], 64, 0, 0) == -1          # null y
     # a split matrix needs a workspace
     big = [(0, 16, 8192)]
     need = codec.gemm_workspace_bytes(big, 2)
