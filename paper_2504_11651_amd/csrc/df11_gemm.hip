@@ -13,6 +13,8 @@
 //     issues v_mfma_f32_16x16x32_bf16 twice per 16-token slice; A (tokens)
 //     and B (features) use the same assignment of k to lanes, so the dot
 //     products cover each k once whatever order the unit sums in;
+//   - up to 3 tokens each wave reads its activations from memory; from 4,
+//     a workgroup of 4 waves stages each 256-k activation slab in LDS once;
 //   - a matrix is split into k ranges of about 1024 columns (up to 32
 //     tokens) or 4096 columns, or half that where it evens out the work per
 //     CU (more tokens); each range of a split matrix writes fp32 partial
