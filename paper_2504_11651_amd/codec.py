@@ -247,6 +247,8 @@ class DeviceStream:
     def __init__(self, hs: HostStream, device="cuda"):
         import torch
         dev = torch.device(device)
+        if dev.type != "cuda":
+            raise ValueError(f"a device stream lives in GPU memory, not on {dev}")
         self.exp = torch.from_numpy(hs.exp).to(dev)
         self.sm = torch.from_numpy(hs.sm).to(dev)
         self.gaps = torch.from_numpy(hs.gaps).to(dev)
@@ -254,7 +256,7 @@ class DeviceStream:
         self.tables = torch.from_numpy(hs.tables).to(dev)
         self.sizes = Sizes.from_buffer_copy(hs.sizes)
         self.layout = Layout.from_buffer_copy(hs.layout)
-        self.device = dev
+        self.device = self.exp.device  # with its index
         self._st = Stream(self.exp.data_ptr(), self.sm.data_ptr(), self.gaps.data_ptr(),
                           self.block_pos.data_ptr(), self.tables.data_ptr(), self.sizes,
                           self.layout)
@@ -283,6 +285,13 @@ def launch_shape(ds: DeviceStream):
     return int(g.value), int(b.value), int(l.value)
 
 
+def _on_device(t, device, what: str):
+    """The library dereferences these pointers on the GPU: a host tensor or
+    one on another GPU would fault there, so it is refused here."""
+    if t.device != device:
+        raise ValueError(f"{what} must be on {device}, not {t.device}")
+
+
 def decode_block(ds: DeviceStream, out=None, stream=None):
     """Decode into ``out`` (a bfloat16 device tensor of n_elems, 16-byte aligned;
     allocated when None) on ``stream`` (default: torch's current stream)."""
@@ -292,6 +301,7 @@ def decode_block(ds: DeviceStream, out=None, stream=None):
         out = torch.empty(n, dtype=torch.bfloat16, device=ds.device)
     if out.numel() < n or out.element_size() != 2 or not out.is_contiguous():
         raise ValueError("out must be a contiguous 2-byte tensor with n_elems elements")
+    _on_device(out, ds.device, "out")
     if stream is None:
         stream = torch.cuda.current_stream(ds.device)
     handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
@@ -317,8 +327,8 @@ def gemm_workspace_bytes(mats, tokens: int) -> int:
     return int(out.value)
 
 
-def _gemm_marshal(mats, xs, ys, workspace):
-    if not (len(mats) == len(xs) == len(ys)):
+def _gemm_marshal(mats, xs, ys, workspace, device):
+    if not (len(mats) == len(xs) == len(ys)) or not mats:
         raise ValueError("one activation and one output tensor per matrix")
     tokens = int(xs[0].shape[0])
     for (off, rows, cols), x, y in zip(mats, xs, ys):
@@ -326,6 +336,10 @@ def _gemm_marshal(mats, xs, ys, workspace):
             raise ValueError("x[m] must be a contiguous bf16 tensor of shape (tokens, cols)")
         if tuple(y.shape) != (tokens, rows) or y.element_size() != 4 or not y.is_contiguous():
             raise ValueError("y[m] must be a contiguous fp32 tensor of shape (tokens, rows)")
+        _on_device(x, device, "x[m]")
+        _on_device(y, device, "y[m]")
+    if workspace is not None:
+        _on_device(workspace, device, "workspace")
     xp = (ctypes.c_void_p * len(xs))(*[x.data_ptr() for x in xs])
     yp = (ctypes.c_void_p * len(ys))(*[y.data_ptr() for y in ys])
     ws_ptr = workspace.data_ptr() if workspace is not None else 0
@@ -343,7 +357,11 @@ def _handle(stream, device):
 def block_gemm(weights, mats, xs, ys, workspace=None, stream=None):
     """ys[m] = xs[m] @ W_m^T for the matrices (offset, rows, cols) of the BF16
     block ``weights`` (device tensor), fp32 results written into ys."""
-    m, xp, yp, tokens, ws_ptr, ws_bytes = _gemm_marshal(mats, xs, ys, workspace)
+    if weights.element_size() != 2 or not weights.is_contiguous():
+        raise ValueError("weights must be a contiguous bf16 tensor")
+    if weights.device.type != "cuda":
+        raise ValueError(f"weights must be on a GPU, not {weights.device}")
+    m, xp, yp, tokens, ws_ptr, ws_bytes = _gemm_marshal(mats, xs, ys, workspace, weights.device)
     _check(lib().df11_block_gemm(ctypes.c_void_p(weights.data_ptr()), weights.numel(), m,
                                  len(mats), xp, tokens, yp, ctypes.c_void_p(ws_ptr), ws_bytes,
                                  ctypes.c_void_p(_handle(stream, weights.device))),
@@ -354,9 +372,11 @@ def block_gemm(weights, mats, xs, ys, workspace=None, stream=None):
 def block_forward(ds: DeviceStream, weights_out, mats, xs, ys, workspace=None, stream=None):
     """Decode ``ds`` into ``weights_out`` (bf16 device tensor of n_elems), then
     block_gemm on it, all on one stream."""
-    if weights_out.numel() < ds.n_elems or weights_out.element_size() != 2:
-        raise ValueError("weights_out must be a 2-byte tensor with n_elems elements")
-    m, xp, yp, tokens, ws_ptr, ws_bytes = _gemm_marshal(mats, xs, ys, workspace)
+    if (weights_out.numel() < ds.n_elems or weights_out.element_size() != 2 or
+            not weights_out.is_contiguous()):
+        raise ValueError("weights_out must be a contiguous 2-byte tensor with n_elems elements")
+    _on_device(weights_out, ds.device, "weights_out")
+    m, xp, yp, tokens, ws_ptr, ws_bytes = _gemm_marshal(mats, xs, ys, workspace, ds.device)
     _check(lib().df11_block_forward(ctypes.byref(ds.struct()),
                                     ctypes.c_void_p(weights_out.data_ptr()), m, len(mats), xp,
                                     tokens, yp, ctypes.c_void_p(ws_ptr), ws_bytes,
@@ -380,16 +400,19 @@ def block_gemv(ds: DeviceStream, mats, xs, ys, workspace=None, stream=None):
     ``ds`` decoded on chip (never written out).  xs[m]: bf16 (cols,) or
     (1, cols); ys[m]: fp32 (rows,) or (1, rows)."""
     import torch
-    if not (len(mats) == len(xs) == len(ys)):
+    if not (len(mats) == len(xs) == len(ys)) or not mats:
         raise ValueError("one activation and one output tensor per matrix")
     for (off, rows, cols), x, y in zip(mats, xs, ys):
         if x.numel() != cols or x.element_size() != 2 or not x.is_contiguous():
             raise ValueError("x[m] must be a contiguous bf16 tensor of cols elements")
         if y.numel() != rows or y.element_size() != 4 or not y.is_contiguous():
             raise ValueError("y[m] must be a contiguous fp32 tensor of rows elements")
+        _on_device(x, ds.device, "x[m]")
+        _on_device(y, ds.device, "y[m]")
     if workspace is None:
         workspace = torch.empty(max(gemv_workspace_bytes(ds, mats) // 4, 4), dtype=torch.float32,
                                 device=ds.device)
+    _on_device(workspace, ds.device, "workspace")
     xp = (ctypes.c_void_p * len(xs))(*[x.data_ptr() for x in xs])
     yp = (ctypes.c_void_p * len(ys))(*[y.data_ptr() for y in ys])
     _check(lib().df11_block_gemv(ctypes.byref(ds.struct()), _mats(mats), len(mats), xp, yp,

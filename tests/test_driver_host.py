@@ -188,3 +188,20 @@ def test_gemv_rejects_other_layouts_and_bad_buffers():
     assert codec.lib().df11_gemv_workspace_bytes(ctypes.byref(st), codec._mats(mats), 1,
                                                  ctypes.byref(out)) == 0
     assert out.value == need
+
+
+def test_binding_refuses_host_tensors():
+    # the library dereferences every pointer on the GPU; the binding refuses
+    # host tensors before calling it
+    import torch
+    w = np.zeros(4096, np.uint16)
+    hs = codec.encode(w)
+    with pytest.raises(ValueError):
+        codec.to_device(hs, "cpu")
+    weights = torch.zeros(1024, dtype=torch.bfloat16)
+    x = torch.zeros((1, 64), dtype=torch.bfloat16)
+    y = torch.zeros((1, 16), dtype=torch.float32)
+    with pytest.raises(ValueError):
+        codec.block_gemm(weights, [(0, 16, 64)], [x], [y])
+    with pytest.raises(ValueError):
+        codec.block_gemm(weights, [], [], [])

@@ -118,3 +118,22 @@ def test_block_forward_rejects_before_decoding():
         codec.block_forward(ds, work.view(torch.bfloat16), [(8, 16, 64)], xs, ys)  # past the end
     torch.cuda.synchronize()
     assert int((work == 0x5A5A).sum()) == w.size  # nothing was decoded
+
+
+def test_binding_refuses_host_tensors():
+    # host tensors are refused before anything is enqueued
+    import torch
+    w, mats = make_block([(16, 2048)], 31)
+    ds = codec.to_device(codec.encode(w), "cuda")
+    with pytest.raises(ValueError):
+        codec.decode_block(ds, torch.empty(w.size, dtype=torch.bfloat16))
+    x = torch.zeros((1, 2048), dtype=torch.bfloat16)
+    y = torch.zeros((1, 16), dtype=torch.float32)
+    work = torch.empty(w.size, dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(ValueError):
+        codec.block_forward(ds, work, mats, [x], [y.cuda()])
+    with pytest.raises(ValueError):
+        codec.block_forward(ds, work, mats, [x.cuda()], [y])
+    with pytest.raises(ValueError):
+        codec.block_gemv(ds, mats, [x.cuda().reshape(-1)], [y.reshape(-1)])
+    torch.cuda.synchronize()
