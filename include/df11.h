@@ -180,8 +180,11 @@ typedef struct {
 } df11_matrix;
 
 /* Device workspace bytes df11_block_gemm / df11_block_forward need for these
- * matrices at this many tokens (partial sums of matrices whose cols are
- * split across workgroups; 0 when none is).  Host, no device access. */
+ * matrices at this many tokens: room for the fp32 partial sums of the
+ * matrices whose cols are split into k ranges (0 when none is).  Above 32
+ * tokens the split is chosen per device to balance its compute units; the
+ * value covers every choice, so it depends only on the shapes.  Host, no
+ * device access. */
 int df11_gemm_workspace_bytes(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens,
                               uint64_t *bytes);
 
