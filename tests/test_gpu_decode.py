@@ -120,3 +120,37 @@ def test_misaligned_output_is_rejected():
     ws = torch.empty(2000, dtype=torch.bfloat16, device="cuda")
     with pytest.raises(codec.DF11Error):
         codec.decode_block(ds, ws[1:1001])
+
+
+def _random_case(seed: int):
+    """Seeded random stream: log-uniform size and scale, a random share of
+    special values and exact zeros, a random launch layout and code cap."""
+    rng = np.random.default_rng(1000 + seed)
+    n = int(np.exp(rng.uniform(0.0, np.log(2_000_000))))
+    sigma = float(np.exp(rng.uniform(np.log(1e-4), np.log(10.0))))
+    w = synth.gaussian(max(n, 1), sigma, 2000 + seed)
+    k = int(rng.integers(0, 3))
+    if k >= 1:  # some special values (Inf, NaN payloads, subnormals, huge)
+        sv = synth.special_values(max(n // 50, 1), 3000 + seed)
+        w[rng.integers(0, w.size, sv.size)] = sv
+    if k == 2:  # and exact zeros
+        w[rng.integers(0, w.size, max(w.size // 100, 1))] = 0
+    lay = LAYOUTS[int(rng.integers(0, len(LAYOUTS)))]
+    cap = int(rng.choice([24, 32]))
+    return w, lay, cap
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_streams_round_trip(seed):
+    w, lay, cap = _random_case(seed)
+    hs = codec.encode(w, layout=codec.make_layout(*lay), max_code_len=cap)
+    assert codec.validate(hs) == 0
+    if w.size <= 200_000:  # the library's stream is the oracle's, byte for byte
+        st = oracle.compress(w, cap, 8, lay[1])
+        assert np.array_equal(st["exp"], hs.exp)
+        assert np.array_equal(st["gaps_packed"], hs.gaps)
+        assert np.array_equal(st["block_pos"], hs.block_pos)
+    got = gpu_decode(hs, 0x2D2D)
+    bad = np.flatnonzero(got != w)
+    assert bad.size == 0, f"n={w.size} layout={lay} cap={cap}: {bad.size} mismatches, " \
+                          f"first {bad[:8].tolist()}"
