@@ -137,3 +137,25 @@ def test_binding_refuses_host_tensors():
     with pytest.raises(ValueError):
         codec.block_gemv(ds, mats, [x.cuda().reshape(-1)], [y.reshape(-1)])
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_blocks_forward(seed):
+    """Seeded random matrix lists and token counts through decode-then-products:
+    every output within the bound of the oracle's float64 product, and bit for
+    bit the products on the uncompressed weights."""
+    import torch
+    rng = np.random.default_rng(500 + seed)
+    shapes = [(16 * int(rng.integers(1, 17)), 64 * int(rng.integers(1, 65)))
+              for _ in range(int(rng.integers(1, 5)))]
+    tokens = int(rng.integers(1, 65))
+    w, mats = make_block(shapes, 600 + seed)
+    ds = codec.to_device(codec.encode(w), "cuda")
+    xs = [synth.activations(tokens, c, 700 + seed, m) for m, (_, _, c) in enumerate(mats)]
+    work = torch.empty(w.size, dtype=torch.bfloat16, device="cuda")
+    y_dec = run_gemm(None, mats, xs, weights_out=work, ds=ds)
+    w_dev = torch.from_numpy(w.view(np.int16)).cuda().view(torch.bfloat16)
+    y_raw = run_gemm(w_dev, mats, xs)
+    for p, q in zip(y_dec, y_raw):
+        assert np.array_equal(p.view(np.uint32), q.view(np.uint32)), f"shapes {shapes} t={tokens}"
+    check_against_oracle(w, mats, xs, y_dec)

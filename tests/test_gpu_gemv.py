@@ -124,3 +124,23 @@ def test_block_gemv_llama3_8b_block_sampled():
         yb = yb.cpu().numpy()[0]
         rel = np.linalg.norm(y - yb) / np.linalg.norm(yb)
         assert rel <= 1e-5, rel
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_random_streams_gemv(seed):
+    """Seeded random matrix lists (2 to 64 rows, so at least 4096 weights;
+    2048 to 5120 columns; gaps of weights outside every matrix) through the
+    fused path: every output within the bound of the oracle's float64
+    product, run to run identical."""
+    rng = np.random.default_rng(800 + seed)
+    k = int(rng.integers(1, 5))
+    shapes = [(int(rng.integers(2, 65)), 64 * int(rng.integers(32, 81))) for _ in range(k)]
+    gaps = tuple(8 * int(rng.integers(0, 700)) if rng.random() < 0.5 else 0 for _ in range(k))
+    w, mats = make_stream(shapes, 900 + seed, gaps=gaps)
+    ds = codec.to_device(codec.encode(w), "cuda")
+    xs_h = [synth.activations(1, c, 950 + seed, i) for i, (_, _, c) in enumerate(mats)]
+    ys = run_gemv(ds, mats, xs_h)
+    check_oracle(w, mats, xs_h, ys)
+    ys2 = run_gemv(ds, mats, xs_h)
+    for a, b in zip(ys, ys2):
+        assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
