@@ -50,7 +50,7 @@ __global__ __launch_bounds__(64 * W) void df11_decode_wave_kernel(DecodeArgs a) 
     extern __shared__ __align__(16) uint8_t lds[];
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
-    const uint32_t wave = tid >> 6;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // block indices stay scalar
     stage_table_blob(a, lds, tid, 64 * W);
     const Tables tb = stage_tables(a, lds);
     uint8_t *buf = lds + a.table_lds_bytes + wave * a.buf_bytes;
@@ -164,6 +164,11 @@ std::mutex g_mu;
 std::vector<DeviceInfo> g_dev;
 
 constexpr uint32_t kWaveChoices[4] = {4, 8, 12, 16};
+// Waves per SIMD for a long stream: 5 beats 4 and 6 (a sixth adds contention
+// for memory and LDS, not throughput).  A short stream takes every wave that
+// fits when that removes a round of blocks per wave (its tail dominates).
+constexpr uint64_t kLongWavesPerSimd = 5;
+constexpr uint64_t kShortRounds = 4;
 constexpr size_t kMaxShapes = 64;  // cached launch shapes per device
 
 KernelFn wave_kernel(uint32_t W) {
@@ -261,8 +266,17 @@ int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *bloc
     *block = found->block;
     *lds = found->lds;
     const uint64_t W = found->waves_per_group;
-    const uint64_t blocks_needed = (s->sizes.num_blocks + W - 1) / W;
-    uint64_t g = static_cast<uint64_t>(di.cus) * found->per_cu;
+    const uint64_t nb = s->sizes.num_blocks;
+    const uint64_t blocks_needed = (nb + W - 1) / W;
+    uint64_t per_cu = found->per_cu;
+    const uint64_t cap = kLongWavesPerSimd * 4 / W;  // 4 SIMDs per CU
+    if (T == 64 && cap >= 1 && per_cu > cap) {
+        const uint64_t cus = static_cast<uint64_t>(di.cus);
+        const uint64_t rounds_all = (nb + cus * per_cu * W - 1) / (cus * per_cu * W);
+        const uint64_t rounds_cap = (nb + cus * cap * W - 1) / (cus * cap * W);
+        if (!(rounds_all < rounds_cap && rounds_all <= kShortRounds)) per_cu = cap;
+    }
+    uint64_t g = static_cast<uint64_t>(di.cus) * per_cu;
     if (g > blocks_needed) g = blocks_needed;
     *grid = static_cast<uint32_t>(g ? g : 1);
     return DF11_OK;
