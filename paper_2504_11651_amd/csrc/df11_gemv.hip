@@ -217,7 +217,7 @@ __global__ __launch_bounds__(64 * W) void df11_gemv_wave_kernel(GemvArgs g) {
     extern __shared__ __align__(16) uint8_t lds[];
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
-    const uint32_t wave = tid >> 6;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // block indices stay scalar
     stage_table_blob(a, lds, tid, 64 * W);
     const Tables tb = stage_tables(a, lds);
     uint8_t *buf = lds + a.table_lds_bytes + wave * a.buf_bytes;
