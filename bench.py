@@ -1,12 +1,21 @@
 """Benchmark: DFloat11 block decompression on one MI355X.
 
-One step = decode one Llama-3-8B-shaped transformer block (q, k, v, o, gate,
-up, down concatenated: 218,103,808 BF16 weights) from its DFloat11 stream,
-resident in HBM, into a reused BF16 workspace -- the whole decode path in
-one launch.  Prints one JSON line.
+One step = decode one transformer block from its DFloat11 stream, resident in
+HBM, into a reused BF16 workspace: the whole decode path in one launch.  The
+default workload is the largest single-GPU block, a Llama-3.1-70B-shaped block
+(q, k, v, o, gate, up, down concatenated: 855,638,016 BF16 weights); the
+4096x4096 matrix, the Llama-3-8B-shaped block and the heavy-tailed block are
+timed the same way and reported under "per_config".  Prints one JSON line.
 
-  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
-                  [--tokens T] [--no-cpu-baseline] [--calib] [--no-cold]
+Timing: --warmup launches, then back-to-back launches for at least
+--settle-ms of GPU time (clocks at their loaded state), then --steps timed
+launches, each after a 1 GiB read that evicts the last-level cache and the
+L2 and between its own HIP events; the median is the headline, min, max and
+the warm back-to-back mean are reported beside it.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--settle-ms MS]
+                  [--workload NAME] [--tokens T] [--no-per-config]
+                  [--no-cpu-baseline] [--calib]
 
 --workload llama3_8b_stack times the decode-then-products driver instead: 32
 blocks resident in compressed form, one step = decode one block into a reused
@@ -102,6 +111,7 @@ def run_stack(args) -> int:
     def timed(fn, steps):
         for i in range(args.warmup):
             fn(i)
+        settle(lambda: fn(0), stream, args.settle_ms)
         torch.cuda.synchronize()
         s_ev, e_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t_0 = time.perf_counter()
@@ -265,23 +275,165 @@ def cpu_baseline(hs, w, min_seconds: float = 10.0, max_reps: int = 16) -> dict:
             "weights_per_s": round(n * reps / t, 1)}
 
 
+# Per-config results of the default run: the largest single-GPU block is the
+# headline, the other block configurations are reported beside it.
+HEADLINE = "llama31_70b_block"
+PER_CONFIG = ("matrix_4096", "llama3_8b_block", "heavy_tailed_block")
+
+
+def settle(fn, stream, min_ms: float, max_launches: int = 20000) -> dict:
+    """Back-to-back launches until at least min_ms of GPU time has passed, so
+    the clocks are at their loaded state before anything is timed, whatever
+    --warmup says.  Batches double from 1 to 64 launches; the first and last
+    batch's mean launch time show how far the GPU had to ramp."""
+    import torch
+    total, launches, batch, first, last = 0.0, 0, 1, None, None
+    while total < min_ms and launches < max_launches:
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record(stream)
+        for _ in range(batch):
+            fn()
+        e.record(stream)
+        e.synchronize()
+        ms = s.elapsed_time(e)
+        first = ms / batch if first is None else first
+        last = ms / batch
+        total += ms
+        launches += batch
+        batch = min(2 * batch, 64)
+    return {"ms": round(total, 1), "launches": launches, "first_launch_ms": round(first, 5),
+            "last_batch_mean_ms": round(last, 5)}
+
+
+def cold_and_warm(fn, stream, steps: int, flush) -> dict:
+    """§ timing protocol: `steps` launches, each after a read of `flush` (1 GiB:
+    evicts the 256 MB last-level cache and the L2) and bracketed by its own
+    HIP event pair on the launch stream; then `steps` back-to-back launches
+    under one event pair (warm, a note).  Returns launch times in ms."""
+    import torch
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs = []
+    for _ in range(steps):
+        flush.sum()
+        s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        s.record(stream)
+        fn()
+        e.record(stream)
+        evs.append((s, e))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    cold = np.array([s.elapsed_time(e) for s, e in evs])
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s.record(stream)
+    for _ in range(steps):
+        fn()
+    e.record(stream)
+    torch.cuda.synchronize()
+    return {"cold": cold, "timed_region_s": wall, "warm_mean": s.elapsed_time(e) / steps}
+
+
+def measure_decode(name: str, w: np.ndarray, lay, args, dev, flush, full: bool) -> dict:
+    """Encode, upload, check bit-exactness, settle, then time the decode of
+    one workload.  Returns the bench record's fields for it."""
+    import torch
+    from paper_2504_11651_amd import codec
+    t0 = time.perf_counter()
+    hs = codec.encode(w, layout=lay)
+    t_enc = time.perf_counter() - t0
+    assert codec.validate(hs) == 0
+    ds = codec.to_device(hs, dev)
+    n = w.size
+    out = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    ref = torch.from_numpy(w.view(np.int16)).to(dev)
+    out.view(torch.int16).fill_(0x5555)
+    codec.decode_block(ds, out, stream=stream)
+    torch.cuda.synchronize()
+    bit_exact = bool(torch.equal(out.view(torch.int16), ref))
+    assert bit_exact, f"{name}: decode is not bit-exact"
+    del ref
+
+    fn = lambda: codec.decode_block(ds, out, stream=stream)
+    for _ in range(args.warmup):
+        fn()
+    st = settle(fn, stream, args.settle_ms)
+    t = cold_and_warm(fn, stream, args.steps, flush)
+    cold = t["cold"]
+    z = hs.sizes
+    read_bytes = hs.compressed_bytes
+    algo = read_bytes + 2 * n
+    med = float(np.median(cold))
+    achieved = algo / (med * 1e-3) / 1e9
+    traffic = profiled_traffic(name, lay)
+    rec = {
+        "weights": n,
+        "bit_exact": bit_exact,
+        "ms": {"cold_median": round(med, 5), "cold_min": round(float(cold.min()), 5),
+               "cold_max": round(float(cold.max()), 5), "cold_mean": round(float(cold.mean()), 5),
+               "warm_mean": round(t["warm_mean"], 5)},
+        "bf16_gbs": round(2.0 * n / (med * 1e-3) / 1e9, 2),
+        "weights_per_s": round(n / (med * 1e-3), 1),
+        "achieved_gbs": round(achieved, 1),
+        "frac": round(achieved / HBM_PEAK_GBS, 4),
+        "traffic": None if traffic is None else round(traffic),
+        "bytes_per_launch": {"read": read_bytes, "write": 2 * n, "algorithmic": algo},
+        "compression": {"bits_per_weight": round(8 + z.total_bits / n, 4),
+                        "ratio": round(read_bytes / (2.0 * n), 4),
+                        "max_code_len": int(z.max_code_len)},
+        "settle": st,
+        "host_s": {"encode": round(t_enc, 2)},
+    }
+    if full:
+        grid, block, lds = codec.launch_shape(ds)
+        cus = torch.cuda.get_device_properties(dev).multi_processor_count
+        rec["launch"] = {"grid": grid, "block": block, "lds_bytes": lds,
+                         "waves_per_simd": round(grid * block / 64 / (4 * cus), 2)}
+        rec["timed_region_s"] = t["timed_region_s"]
+        rec["_hs"] = hs
+    del ds, out
+    torch.cuda.empty_cache()
+    return rec
+
+
+def device_copy_gbs(dev, stream) -> float:
+    """Context: what a plain device-to-device copy (read + write, no decode)
+    sustains, 512 MiB each way (twice the last-level cache), event timed."""
+    import torch
+    src = torch.empty(1 << 29, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    for _ in range(20):
+        dst.copy_(src)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    gbs = 2.0 * src.numel() * 20 / (c0.elapsed_time(c1) * 1e-3) / 1e9
+    del src, dst
+    return gbs
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=500)
-    ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default="llama3_8b_block",
-                    help="llama3_8b_block, heavy_tailed_block, llama31_70b_block, matrix_4096, "
-                         "llama3_8b_stack (decode + 7 products per step)")
+    ap.add_argument("--steps", type=int, default=20,
+                    help="timed launches, each after a cache eviction")
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--settle-ms", type=float, default=300.0,
+                    help="back-to-back launches before timing, in GPU milliseconds")
+    ap.add_argument("--workload", default=HEADLINE,
+                    help="llama31_70b_block (default), llama3_8b_block, heavy_tailed_block, "
+                         "matrix_4096, llama3_8b_stack (decode + 7 products per step)")
     ap.add_argument("--tokens", type=int, default=64, help="activation rows (llama3_8b_stack)")
     ap.add_argument("--threads", type=int, default=None, help="threads per block T")
     ap.add_argument("--lut-bits", type=int, default=None)
+    ap.add_argument("--no-per-config", action="store_true",
+                    help="time only --workload, not the other block configurations")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib", action="store_true",
                     help="also run a plain device copy of known size (PMC calibration)")
-    ap.add_argument("--no-cold", action="store_true",
-                    help="skip the extra cold-cache launches (each after a 1 GiB read that "
-                         "evicts the 256 MB last-level cache and the L2)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -296,70 +448,28 @@ def main() -> int:
     if args.workload == "llama3_8b_stack":
         return run_stack(args)
     dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    lay = codec.make_layout(8, args.threads, args.lut_bits)
+    flush = torch.ones(1 << 28, dtype=torch.int32, device=dev)  # 1 GiB
+
+    per_config = {}
+    if not args.no_per_config:
+        for name in PER_CONFIG:
+            if name == args.workload:
+                continue
+            wk = workload(name)
+            per_config[name] = measure_decode(name, wk, lay, args, dev, flush, full=False)
+            del wk
+
     t0 = time.perf_counter()
     w = workload(args.workload)
     t_gen = time.perf_counter() - t0
-    lay = codec.make_layout(8, args.threads, args.lut_bits)
-    t0 = time.perf_counter()
-    hs = codec.encode(w, layout=lay)
-    t_enc = time.perf_counter() - t0
-    assert codec.validate(hs) == 0
-    ds = codec.to_device(hs, dev)
-    n = w.size
-    out = torch.empty(n, dtype=torch.bfloat16, device=dev)
-    ref = torch.from_numpy(w.view(np.int16)).to(dev)
-    stream = torch.cuda.current_stream(dev)
-
-    # bit-exact before timing
-    codec.decode_block(ds, out)
-    torch.cuda.synchronize()
-    bit_exact = bool(torch.equal(out.view(torch.int16), ref))
-    assert bit_exact, "decode is not bit-exact"
-    del ref
-
-    for _ in range(args.warmup):
-        codec.decode_block(ds, out)
-    torch.cuda.synchronize()
-
-    # timed region: K back-to-back decodes; HIP events on the decode stream
-    # bracket the same region (kernel time per launch = event span / K)
-    ev_start = torch.cuda.Event(enable_timing=True)
-    ev_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev_start.record(stream)
-    for _ in range(args.steps):
-        codec.decode_block(ds, out, stream=stream)
-    ev_end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    kern_ms = ev_start.elapsed_time(ev_end) / args.steps
-
-    # per-launch spread (separate pass, one event pair per launch)
-    per = []
-    for _ in range(min(args.steps, 20)):
-        s_ev, e_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        s_ev.record(stream)
-        codec.decode_block(ds, out, stream=stream)
-        e_ev.record(stream)
-        per.append((s_ev, e_ev))
-    torch.cuda.synchronize()
-    ev_ms = np.array([s_ev.elapsed_time(e_ev) for s_ev, e_ev in per])
-
-    cold = None
-    if not args.no_cold:
-        scratch = torch.ones(1 << 28, dtype=torch.int32, device=dev)  # 1 GiB
-        cms = []
-        for i in range(max(5, min(args.steps // 5, 20))):
-            scratch.sum()  # evicts the MALL and L2 by reading 1 GiB (no dirty lines left)
-            s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            s.record(stream)
-            codec.decode_block(ds, out)
-            e.record(stream)
-            torch.cuda.synchronize()
-            cms.append(s.elapsed_time(e))
-        del scratch
-        cold = float(np.median(cms))
+    head = measure_decode(args.workload, w, lay, args, dev, flush, full=True)
+    hs = head.pop("_hs")
+    timed_region_s = head.pop("timed_region_s")
+    launch = head.pop("launch")
+    del flush
+    torch.cuda.empty_cache()
 
     if args.calib:
         # plain copy kernel of known size for scaling FETCH_SIZE / WRITE_SIZE counters
@@ -369,44 +479,18 @@ def main() -> int:
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    copy_gbs = device_copy_gbs(dev, stream)
 
-    # context: what a plain device-to-device copy (read + write, no decode)
-    # sustains on this GPU, 512 MiB each way (twice the last-level cache),
-    # same event timing
-    src = torch.empty(1 << 29, dtype=torch.uint8, device=dev).fill_(1)
-    dst = torch.empty_like(src)
-    for _ in range(3):
-        dst.copy_(src)
-    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    c0.record(stream)
-    for _ in range(20):
-        dst.copy_(src)
-    c1.record(stream)
-    torch.cuda.synchronize()
-    copy_gbs = 2.0 * src.numel() * 20 / (c0.elapsed_time(c1) * 1e-3) / 1e9
-    del src, dst
-
-    z = hs.sizes
-    exp_bytes_exact = (int(z.total_bits) + 7) // 8
-    read_bytes = exp_bytes_exact + n + int(z.gap_bytes) + int(z.block_pos_bytes) + \
-        int(z.table_bytes)
-    write_bytes = 2 * n
-    algo_bytes = read_bytes + write_bytes
-    achieved = algo_bytes / (kern_ms * 1e-3) / 1e9
-    ms_per_step = wall * 1e3 / args.steps
-    value = 2.0 * n / (ms_per_step * 1e-3) / 1e9
-    grid, block, lds = codec.launch_shape(ds)
-    cus = torch.cuda.get_device_properties(dev).multi_processor_count
-    traffic = profiled_traffic(args.workload, lay)
-
+    n = w.size
+    med = head["ms"]["cold_median"]
     rec = {
         "metric": METRIC,
-        "value": round(value, 2),
+        "value": head["bf16_gbs"],
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step": med,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -419,35 +503,31 @@ def main() -> int:
             "layout": {"bytes_per_thread": int(lay.bytes_per_thread),
                        "threads_per_block": int(lay.threads_per_block),
                        "lut_bits": int(lay.lut_bits)},
-            "launch": {"grid": grid, "block": block, "lds_bytes": lds,
-                       "waves_per_simd": round(grid * block / 64 / (4 * cus), 2)},
+            "launch": launch,
+            "timing": "per step: 1 GiB read evicts the MALL and L2, then one decode launch "
+                      "between its own HIP events; ms_per_step and value use the median",
         },
         "roofline": {
             "bound": "hbm",
-            "achieved": round(achieved, 1),
+            "achieved": head["achieved_gbs"],
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None if traffic is None else round(traffic),
+            "frac": head["frac"],
+            "traffic": head["traffic"],
         },
-        "pct_hbm_roofline": round(100.0 * achieved / HBM_PEAK_GBS, 2),
+        "bit_exact": head["bit_exact"],
+        "kernel_ms": head["ms"],
+        "weights_per_s": head["weights_per_s"],
+        "settle": head["settle"],
+        "timed_region_s": round(timed_region_s, 4),
         "device_copy_gbs": round(copy_gbs, 1),
-        "achieved_over_device_copy": round(achieved / copy_gbs, 4),
-        "weights_per_s": round(n / (ms_per_step * 1e-3), 1),
-        "bit_exact": bit_exact,
-        "kernel_ms": {"mean_in_timed_region": round(kern_ms, 5),
-                      "single_launch_median": round(float(np.median(ev_ms)), 5),
-                      "single_launch_min": round(float(ev_ms.min()), 5),
-                      "single_launch_max": round(float(ev_ms.max()), 5)},
-        "bytes_per_step": {"read": read_bytes, "write": write_bytes, "algorithmic": algo_bytes},
-        "compression": {"bits_per_weight": round(8 + z.total_bits / n, 4),
-                        "ratio": round((read_bytes) / (2.0 * n), 4),
-                        "max_code_len": int(z.max_code_len)},
-        "host_s": {"generate": round(t_gen, 2), "encode": round(t_enc, 2)},
+        "achieved_over_device_copy": round(head["achieved_gbs"] / copy_gbs, 4),
+        "bytes_per_step": head["bytes_per_launch"],
+        "compression": head["compression"],
+        "host_s": {"generate": round(t_gen, 2), **head["host_s"]},
     }
-    if cold is not None:
-        rec["cold_cache_kernel_ms_median"] = round(cold, 5)
-        rec["cold_cache_bf16_gbs"] = round(2.0 * n / (cold * 1e-3) / 1e9, 2)
+    if per_config:
+        rec["per_config"] = per_config
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(hs, w)
     print(json.dumps(rec), flush=True)
