@@ -41,7 +41,9 @@
  * functions take host pointers; df11_decode_block, df11_block_gemm and
  * df11_block_forward take device pointers (inside df11_stream, and for the
  * weights, activations, outputs and workspace).  The library keeps no
- * per-call state and allocates no device memory.
+ * per-call state and allocates no device memory; its one device-side array,
+ * the partial sums of df11_block_forward_noalloc, is a fixed-size static
+ * array of DF11_STATIC_SCRATCH_BYTES per GPU.
  *
  * Errors: every function returns DF11_OK (0) or a negative DF11_E_* code;
  * nothing is thrown across the ABI.  df11_strerror names a code.
@@ -217,6 +219,32 @@ int df11_block_forward(const df11_stream *dev, uint16_t *weights_out, const df11
                        uint32_t n_mats, const uint16_t *const *x, uint32_t tokens,
                        float *const *y, void *workspace, uint64_t workspace_bytes,
                        hipStream_t stream);
+
+/* ---- The same, allocating nothing: for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).
+ *
+ * df11_block_forward with the fp32 partial sums held in a fixed array of
+ * DF11_STATIC_SCRATCH_BYTES that the library keeps on each GPU it runs on
+ * until the process ends, instead of a caller workspace.  The caller still
+ * passes the stream, the decoded-weight buffer, activations and outputs.
+ * The array's device address is looked up once per device, on the first
+ * call with that device current; no call allocates device memory.
+ *   returns DF11_E_BUFFER_TOO_SMALL when these matrices at this many tokens
+ *   need more partial sums than the array holds (df11_gemm_workspace_bytes
+ *   > DF11_STATIC_SCRATCH_BYTES): the Llama-3-8B block shapes fit at every
+ *   token count up to DF11_MAX_TOKENS, the Llama-3.1-70B block up to 10;
+ *   otherwise the same arguments, checks and results as df11_block_forward
+ *   (bit-identical outputs).
+ * All calls on one GPU share its array: calls that overlap in time on one
+ * GPU (two streams, two host threads) race on it and must be serialised by
+ * the caller. */
+#define DF11_STATIC_SCRATCH_BYTES (32u << 20)
+
+int df11_block_forward_noalloc(const df11_stream *dev, uint16_t *weights_out,
+                               const df11_matrix *mats, uint32_t n_mats,
+                               const uint16_t *const *x, uint32_t tokens, float *const *y,
+                               hipStream_t stream);
 
 /* ---- Fused decode-and-multiply for one token (decode-time products without
  * a decoded copy of the block: the decompression of Algorithm 1 feeds the

@@ -27,11 +27,12 @@ EXPORTS = (
     "df11_build_codebook", "df11_codebook_from_counts", "df11_encoded_sizes", "df11_encode",
     "df11_build_tables", "df11_validate", "df11_decode_block", "df11_decode_launch_shape",
     "df11_gemm_workspace_bytes", "df11_block_gemm", "df11_block_forward",
-    "df11_gemv_workspace_bytes", "df11_block_gemv", "df11_strerror",
+    "df11_block_forward_noalloc", "df11_gemv_workspace_bytes", "df11_block_gemv", "df11_strerror",
 )
 
 MAX_MATRICES = 8  # DF11_MAX_MATRICES
 MAX_TOKENS = 64   # DF11_MAX_TOKENS
+STATIC_SCRATCH_BYTES = 32 << 20  # DF11_STATIC_SCRATCH_BYTES
 
 
 class Codebook(ctypes.Structure):
@@ -118,6 +119,8 @@ def lib():
                             vp, u64, vp],
         "df11_block_forward": [P(Stream), vp, P(Matrix), ctypes.c_uint32, P(vp), ctypes.c_uint32,
                                P(vp), vp, u64, vp],
+        "df11_block_forward_noalloc": [P(Stream), vp, P(Matrix), ctypes.c_uint32, P(vp),
+                                       ctypes.c_uint32, P(vp), vp],
         "df11_gemv_workspace_bytes": [P(Stream), P(Matrix), ctypes.c_uint32, P(u64)],
         "df11_block_gemv": [P(Stream), P(Matrix), ctypes.c_uint32, P(vp), P(vp), vp, u64, vp],
     }
@@ -382,6 +385,23 @@ def block_forward(ds: DeviceStream, weights_out, mats, xs, ys, workspace=None, s
                                     tokens, yp, ctypes.c_void_p(ws_ptr), ws_bytes,
                                     ctypes.c_void_p(_handle(stream, ds.device))),
            "df11_block_forward")
+    return ys
+
+
+def block_forward_noalloc(ds: DeviceStream, weights_out, mats, xs, ys, stream=None):
+    """block_forward with the partial sums in the library's fixed per-GPU
+    array (no workspace, no device allocation by the library).  Calls that
+    overlap on one GPU race on that array."""
+    if (weights_out.numel() < ds.n_elems or weights_out.element_size() != 2 or
+            not weights_out.is_contiguous()):
+        raise ValueError("weights_out must be a contiguous 2-byte tensor with n_elems elements")
+    _on_device(weights_out, ds.device, "weights_out")
+    m, xp, yp, tokens, _, _ = _gemm_marshal(mats, xs, ys, None, ds.device)
+    _check(lib().df11_block_forward_noalloc(ctypes.byref(ds.struct()),
+                                            ctypes.c_void_p(weights_out.data_ptr()), m,
+                                            len(mats), xp, tokens, yp,
+                                            ctypes.c_void_p(_handle(stream, ds.device))),
+           "df11_block_forward_noalloc")
     return ys
 
 

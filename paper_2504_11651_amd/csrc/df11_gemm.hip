@@ -552,6 +552,29 @@ int launch(const GemmArgs &g, const ReduceArgs &r, hipStream_t stream) {
     return DF11_OK;
 }
 
+// Partial sums of the entry point that allocates nothing: one array per
+// GPU, held until the process ends.  Host code never passes the array's name
+// to a kernel (on the host it is a stand-in, not a device address); it uses
+// the address hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) float scratch[DF11_STATIC_SCRATCH_BYTES / sizeof(float)];
+
+std::mutex g_scratch_mu;
+std::vector<void *> g_scratch;  // device address of `scratch`, per device
+
+int scratch_address(void **out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return DF11_E_HIP;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (g_scratch.size() <= static_cast<size_t>(dev)) g_scratch.resize(dev + 1, nullptr);
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return DF11_E_HIP;
+        g_scratch[dev] = p;
+    }
+    *out = g_scratch[dev];
+    return DF11_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -589,6 +612,23 @@ int df11_block_forward(const df11_stream *dev, uint16_t *weights_out, const df11
     rc = df11_decode_block(dev, weights_out, stream);
     if (rc) return rc;
     return launch(g, r, stream);
+}
+
+int df11_block_forward_noalloc(const df11_stream *dev, uint16_t *weights_out,
+                               const df11_matrix *mats, uint32_t n_mats,
+                               const uint16_t *const *x, uint32_t tokens, float *const *y,
+                               hipStream_t stream) {
+    if (!dev) return DF11_E_INVALID_ARG;
+    int rc = check_mats(mats, n_mats, tokens);
+    if (rc) return rc;
+    // every partial sum is written before it is read: nothing to clear
+    if (4 * workspace_floats(mats, n_mats, tokens) > DF11_STATIC_SCRATCH_BYTES)
+        return DF11_E_BUFFER_TOO_SMALL;
+    void *ws = nullptr;
+    rc = scratch_address(&ws);
+    if (rc) return rc;
+    return df11_block_forward(dev, weights_out, mats, n_mats, x, tokens, y, ws,
+                              DF11_STATIC_SCRATCH_BYTES, stream);
 }
 
 }  // extern "C"
