@@ -27,7 +27,9 @@
 //      8 consecutive outputs per lane and step: one 8-byte PackedSignMantissa
 //      load (issued when the block starts), one 8-byte LDS read, one 16-byte
 //      store; consecutive lanes take consecutive groups, so a wave stores
-//      1 KiB contiguous per instruction.  No per-element gather (the paper
+//      1 KiB contiguous per instruction.  The block's first and last group
+//      may be shared with its neighbours; their elements go out as one
+//      2-byte store over 16 lanes.  No per-element gather (the paper
 //      gathers sign/mantissa per element).
 // Integer work only; no MFMA.
 #include <hip/hip_runtime.h>
@@ -72,6 +74,7 @@ __global__ __launch_bounds__(64 * W) void df11_decode_wave_kernel(DecodeArgs a) 
         if (bn < a.num_blocks) nxt = load_chunk(a, bn, bn * 64u + lane);
         uint2 S[kPre];
         prefetch_sm(a, r, lane, 64u, S);
+        const uint32_t edge_sm = prefetch_edge_sm(a, r, lane);
 
         wave_lds_sync();  // this wave's reads of the previous block are issued
         for (uint32_t i = lane; i < (a.buf_bytes >> 4); i += 64u)
@@ -89,7 +92,7 @@ __global__ __launch_bounds__(64 * W) void df11_decode_wave_kernel(DecodeArgs a) 
         wave_lds_sync();
 
         __builtin_amdgcn_s_setprio(2);
-        assemble_block(a, r, buf, lane, 64u, S);
+        assemble_block(a, r, buf, lane, 64u, S, edge_sm);
         __builtin_amdgcn_s_setprio(0);
         cw = nxt;
         ch = chunk_setup(a, cw, bn * 64u + lane);
@@ -122,6 +125,7 @@ __global__ __launch_bounds__(T) void df11_decode_block_kernel(DecodeArgs a) {
         if (bn < a.num_blocks) nxt = load_chunk(a, bn, bn * T + tid);
         uint2 S[kPre];
         prefetch_sm(a, r, tid, T, S);
+        const uint32_t edge_sm = prefetch_edge_sm(a, r, tid);
 
         __syncthreads();  // tables staged / previous block's buffer consumed
         for (uint32_t i = tid; i < (a.buf_bytes >> 4); i += T)
@@ -138,7 +142,7 @@ __global__ __launch_bounds__(T) void df11_decode_block_kernel(DecodeArgs a) {
         emit_exponents(tb, ch, sy, npk, p_rest, r.shift + before + incl - cnt, buf32, cap);
         __syncthreads();
 
-        assemble_block(a, r, buf, tid, T, S);
+        assemble_block(a, r, buf, tid, T, S, edge_sm);
         cw = nxt;
         ch = chunk_setup(a, cw, bn * T + tid);
         r = block_range(a, cw);

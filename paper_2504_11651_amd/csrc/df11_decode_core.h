@@ -265,9 +265,14 @@ __device__ __forceinline__ void emit_exponents(const Tables &t, const Chunk &ch,
     }
 }
 
-// A block's output range, clamped to the buffer and the tensor.
+// A block's output range, clamped to the buffer and the tensor.  Outputs
+// are handled in 8-element groups aligned to the tensor: group g of the
+// block covers buffer bytes [8g, 8g+8), i.e. outputs g0 + 8g .. g0 + 8g + 7;
+// the block owns buffer bytes [shift, lim).  Only the first and the last
+// group can be partial (shared with the neighbouring block): the groups
+// [full_lo, full_hi) are whole.
 struct Range {
-    uint32_t s, shift, lim, g0, ngroups;
+    uint32_t s, shift, lim, g0, ngroups, full_lo, full_hi;
 };
 
 __device__ __forceinline__ Range block_range(const DecodeArgs &a, const ChunkWords &cw) {
@@ -281,11 +286,13 @@ __device__ __forceinline__ Range block_range(const DecodeArgs &a, const ChunkWor
     r.lim = r.shift + (e - r.s);
     r.g0 = r.s - r.shift;
     r.ngroups = (r.lim + 7u) >> 3;
+    r.full_lo = r.shift ? 1u : 0u;
+    r.full_hi = umax(r.lim >> 3, r.full_lo);
     return r;
 }
 
 __device__ __forceinline__ bool full_group(const Range &r, uint32_t g) {
-    return (g << 3) >= r.shift && (g << 3) + 8u <= r.lim;
+    return g - r.full_lo < r.full_hi - r.full_lo;  // full_lo <= g < full_hi
 }
 
 // Sign/mantissa bytes of groups first, first+step, ... (kPre of them).  The
@@ -301,6 +308,22 @@ __device__ __forceinline__ void prefetch_sm(const DecodeArgs &a, const Range &r,
     }
 }
 
+// Edge elements: threads 0..7 take element t of the block's first group,
+// threads 8..15 element t-8 of its last group.  Buffer byte of thread t's
+// element (inside [0, 8*ngroups) whenever the block has a group).
+__device__ __forceinline__ uint32_t edge_byte(const Range &r, uint32_t t) {
+    return (t < 8u ? 0u : (umax(r.ngroups, 1u) - 1u) << 3) + (t & 7u);
+}
+
+// The sign/mantissa byte of this thread's edge element (threads 0..15),
+// fetched when the block starts like the groups' bytes.
+__device__ __forceinline__ uint32_t prefetch_edge_sm(const DecodeArgs &a, const Range &r,
+                                                     uint32_t t) {
+    uint32_t v = 0;
+    if (t < 16u) v = a.sm[r.g0 + edge_byte(r, t)];
+    return v;
+}
+
 // 8 outputs of group g from its sign/mantissa bytes and the exponent buffer.
 __device__ __forceinline__ uint4 assemble_group(const uint8_t *buf, uint32_t g, uint2 Sg) {
     const uint2 E = reinterpret_cast<const uint2 *>(buf)[g];
@@ -310,57 +333,54 @@ __device__ __forceinline__ uint4 assemble_group(const uint8_t *buf, uint32_t g, 
     return o;
 }
 
-// One 16-byte non-temporal store (the output is written once and not read
-// back by this kernel), or narrower stores for a group that the block shares
-// with its neighbour.
+// One 16-byte non-temporal store of a whole group (the output is written
+// once and not read back by this kernel).
 __device__ __forceinline__ void store_group(const DecodeArgs &a, const Range &r, uint32_t g,
                                             const uint4 &o) {
-    uint16_t *dst = a.out + r.g0 + (g << 3);
-    if (full_group(r, g)) {
-        typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-        const u32x4 ov = {o.x, o.y, o.z, o.w};
-        __builtin_nontemporal_store(ov, reinterpret_cast<u32x4 *>(dst));
-        return;
-    }
-    // elements k in [lo, hi) of the group belong to this block: element
-    // pairs inside go out as one 4-byte store, a lone element as 2 bytes
-    const int lo = static_cast<int>(r.shift) - static_cast<int>(g << 3);
-    const int hi = static_cast<int>(r.lim) - static_cast<int>(g << 3);
-    const uint32_t v[4] = {o.x, o.y, o.z, o.w};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-        const bool in0 = 2 * q >= lo && 2 * q < hi, in1 = 2 * q + 1 >= lo && 2 * q + 1 < hi;
-        if (in0 && in1) {
-            reinterpret_cast<uint32_t *>(dst)[q] = v[q];
-        } else if (in0 || in1) {
-            dst[2 * q + (in1 ? 1 : 0)] = static_cast<uint16_t>(v[q] >> (in1 ? 16 : 0));
-        }
-    }
+    typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 ov = {o.x, o.y, o.z, o.w};
+    __builtin_nontemporal_store(ov, reinterpret_cast<u32x4 *>(a.out + r.g0 + (g << 3)));
 }
 
-// Assemble and store every group of the block: groups first + k*step.  The
-// first kPre use the bytes fetched when the block started.  Loads and stores
-// share one in-order counter on this GPU, so all of those groups are
+// Assemble and store every whole group of the block: groups first + k*step.
+// The first kPre use the bytes fetched when the block started.  Loads and
+// stores share one in-order counter on this GPU, so all of those groups are
 // assembled (their loads waited for) before the first store is issued;
 // otherwise each wait would also wait for the stores issued before it.
+// Then the elements of the (at most two) partial groups that this block
+// owns go out as one 2-byte store instruction over threads 0..15.
 __device__ __forceinline__ void assemble_block(const DecodeArgs &a, const Range &r,
                                                const uint8_t *buf, uint32_t first, uint32_t step,
-                                               const uint2 (&S)[kPre]) {
+                                               const uint2 (&S)[kPre], uint32_t edge_sm) {
     uint4 O[kPre];
 #pragma unroll
     for (int k = 0; k < kPre; ++k) {
         const uint32_t g = first + k * step;
         O[k] = make_uint4(0u, 0u, 0u, 0u);
-        if (g < r.ngroups) O[k] = assemble_group(buf, g, S[k]);
+        if (full_group(r, g)) O[k] = assemble_group(buf, g, S[k]);
     }
 #pragma unroll
     for (int k = 0; k < kPre; ++k) {
         const uint32_t g = first + k * step;
-        if (g < r.ngroups) store_group(a, r, g, O[k]);
+        if (full_group(r, g)) store_group(a, r, g, O[k]);
     }
-    for (uint32_t g = first + kPre * step; g < r.ngroups; g += step)
-        store_group(a, r, g,
-                    assemble_group(buf, g, *reinterpret_cast<const uint2 *>(a.sm + r.g0 + (g << 3))));
+    for (uint32_t g = first + kPre * step; g < r.full_hi; g += step)
+        if (full_group(r, g))
+            store_group(a, r, g,
+                        assemble_group(buf, g, *reinterpret_cast<const uint2 *>(a.sm + r.g0 + (g << 3))));
+    if (first < 16u) {
+        const uint32_t t = first;
+        const uint32_t el = edge_byte(r, t);
+        const uint32_t g = el >> 3;
+        // the last group is taken by threads 8..15 only when it is not also the first
+        const bool mine = r.ngroups != 0u && !full_group(r, g) && (t < 8u || g != 0u) &&
+                          el >= r.shift && el < r.lim;
+        if (mine) {
+            const uint32_t e = buf[el];
+            a.out[r.g0 + el] = static_cast<uint16_t>(((edge_sm & 0x80u) << 8) | (e << 7) |
+                                                     (edge_sm & 0x7Fu));
+        }
+    }
 }
 
 // Workgroups are dispatched to the 8 XCDs round robin and each XCD has its
