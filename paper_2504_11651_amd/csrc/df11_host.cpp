@@ -5,6 +5,7 @@
 // transformer block per CPU thread); here it is parallel over element
 // ranges so large blocks encode in seconds.
 #include <algorithm>
+#include <array>
 #include <atomic>
 #include <cstdint>
 #include <cstring>

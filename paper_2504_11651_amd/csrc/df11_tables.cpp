@@ -2,6 +2,7 @@
 #include "df11_tables.h"
 
 #include <cstring>
+#include <vector>
 
 #include "df11.h"
 
@@ -99,17 +100,46 @@ int build(const uint8_t *len, const uint32_t *code, uint32_t max_len, uint32_t K
 }
 
 int check(const uint8_t *blob, uint32_t K, uint32_t max_len) {
-    if (get32(blob) != kMagic || get32(blob + 4) != K || get32(blob + 8) != max_len)
+    if (get32(blob) != kMagic || get32(blob + 4) != K || get32(blob + 8) != max_len ||
+        max_len > 32)
         return DF11_E_CORRUPT;
-    const uint8_t *ent = blob + kHeaderBytes;
-    for (uint32_t x = 0; x < (1u << K); ++x) {
-        uint32_t meta = get32(ent + 8ull * x + 4);
-        unsigned bits = meta & 0xFF, n = (meta >> 8) & 0xFF, mask = meta >> 16;
-        if (meta == 0) continue;
-        if (n < 1 || n > 4 || bits < 1 || bits > K || !(mask & 1u) || (mask >> K)) return DF11_E_CORRUPT;
-        if (static_cast<unsigned>(__builtin_popcount(mask)) != n) return DF11_E_CORRUPT;
+    // The code the blob describes, read back from its escape arrays: the
+    // canonical codes of length L are [first[L], end[L]) with end[L] =
+    // (lj_last[L] + 1) >> (32 - L) and first[L+1] = 2 * end[L].  Below the
+    // shortest length (first = 0, no code yet) lj_last is 2^32 - 1, which
+    // at the longest length instead means end = 2^L (a complete code).
+    const uint8_t *esc = blob + kHeaderBytes + entry_bytes(K);
+    const uint8_t *sorted = esc + 8 * kEscWords;
+    uint8_t len[256] = {0};
+    uint64_t first = 0, nsym = 0, kraft = 0;  // kraft: sum of 2^(32-L), exact in 64 bits
+    for (unsigned l = 1; l <= max_len; ++l) {
+        const uint32_t lj = get32(esc + 4 * l);
+        const uint64_t end = (first == 0 && lj == 0xFFFFFFFFu && l < max_len)
+                                 ? 0
+                                 : (static_cast<uint64_t>(lj) + 1) >> (32 - l);
+        if (end < first || end > (uint64_t{1} << l)) return DF11_E_CORRUPT;
+        const uint64_t count = end - first;
+        if (nsym + count > 256) return DF11_E_CORRUPT;
+        for (uint64_t i = 0; i < count; ++i) {
+            const uint8_t sym = sorted[nsym + i];
+            // exponents of one length in increasing order, each used once
+            if (len[sym] || (i && sym <= sorted[nsym + i - 1])) return DF11_E_CORRUPT;
+            len[sym] = static_cast<uint8_t>(l);
+        }
+        kraft += count << (32 - l);
+        nsym += count;
+        first = end << 1;
     }
-    return DF11_OK;
+    // a complete prefix code (Kraft sum 1) for two or more symbols; a lone
+    // symbol has the one-bit code 0
+    if (nsym == 0 || (nsym == 1 ? len[sorted[0]] != 1 : kraft != (uint64_t{1} << 32)))
+        return DF11_E_CORRUPT;
+    if (len[sorted[nsym - 1]] != max_len) return DF11_E_CORRUPT;
+    // everything else (the K-bit entries, offsets, padding) follows from the
+    // lengths: rebuild and compare byte for byte
+    std::vector<uint8_t> again(blob_bytes(K));
+    if (build(len, nullptr, max_len, K, again.data()) != DF11_OK) return DF11_E_CORRUPT;
+    return std::memcmp(again.data(), blob, again.size()) ? DF11_E_CORRUPT : DF11_OK;
 }
 
 }  // namespace df11tab

@@ -43,6 +43,10 @@ inline uint64_t blob_bytes(uint32_t lut_bits) { return kHeaderBytes + lds_bytes(
 
 int build(const uint8_t *len, const uint32_t *code, uint32_t max_len, uint32_t lut_bits,
           uint8_t *blob);
+// DF11_OK when the blob is exactly what build() makes for some code book
+// with this table width and longest code: its escape arrays describe a
+// canonical code that is a complete prefix code (Kraft sum 1; one symbol:
+// a one-bit code), and every other byte equals the rebuilt blob's.
 int check(const uint8_t *blob, uint32_t lut_bits, uint32_t max_len);
 
 }  // namespace df11tab

@@ -8,11 +8,6 @@ import pytest
 
 from paper_2504_11651_amd import codec, synth
 
-from conftest import gpu_available
-
-# argument checks only; with a device present the GPU tests cover these paths
-pytestmark = pytest.mark.skipif(gpu_available(), reason="host-only argument checks")
-
 def llama_mats():
     mats, off = [], 0
     for _, r, c in synth.LLAMA3_8B_BLOCK:

@@ -275,6 +275,62 @@ def test_validate_rejects_corruption():
     assert codec.validate(hs) == -4
 
 
+def _table_words(hs):
+    """(entries as uint32 pairs, lj_last[33], offset[33], sorted[256]) views
+    into the stream's table blob (layout of df11_tables.h)."""
+    K = int(hs.layout.lut_bits)
+    body = hs.tables[16:]
+    ent = body[:8 << K].view(np.uint32)
+    esc = body[8 << K:(8 << K) + 264].view(np.uint32)
+    return ent, esc[:33], esc[33:66], body[(8 << K) + 264:(8 << K) + 264 + 256]
+
+
+@pytest.mark.parametrize("what", ["entry_exponent", "entry_meta", "lj_last", "lj_last_top",
+                                  "offset", "sorted_swap", "sorted_dup", "sorted_tail",
+                                  "padding"])
+def test_validate_rejects_corrupt_tables(what):
+    """The table blob must be the canonical tables of a complete prefix code
+    (Kraft sum 1): any single corrupted entry, length boundary, offset or
+    symbol is refused."""
+    hs = _fresh()
+    assert codec.validate(hs) == 0
+    ent, lj, off, srt = _table_words(hs)
+    L = int(hs.sizes.max_code_len)
+    if what == "entry_exponent":
+        ent[2 * 7] ^= 1 << 8           # second exponent of entry 7
+    elif what == "entry_meta":
+        ent[2 * 100 + 1] ^= 1 << 16    # code-start mask of entry 100
+    elif what == "lj_last":
+        lj[3] -= 1 << 29               # length-3 codes end one code earlier
+    elif what == "lj_last_top":
+        lj[L] -= 1 << (32 - L)         # the longest length loses a code: Kraft < 1
+    elif what == "offset":
+        off[4] += 1
+    elif what == "sorted_swap":
+        srt[0], srt[1] = srt[1], srt[0]
+    elif what == "sorted_dup":
+        srt[1] = srt[0]
+    elif what == "sorted_tail":
+        srt[255] = 1                   # past the used symbols: must stay zero
+    elif what == "padding":
+        hs.tables[-1] = 0x5A
+    assert codec.validate(hs) == -4
+
+
+def test_validate_accepts_valid_books():
+    """Complete codes of every shape validate: one symbol (a 1-bit code),
+    two symbols, all 65,536 BF16 patterns (256 symbols), a 32-bit code."""
+    cases = [np.full(1000, 0x3F80, np.uint16), np.array([0x3F80, 0x4000] * 50, np.uint16),
+             synth.all_bf16_patterns()]
+    counts = np.array([1 << (31 - i) if i < 31 else 1 for i in range(32)] + [1], np.uint64)
+    geo = np.repeat((np.arange(33, dtype=np.uint16) + 60) << 7, counts.astype(np.int64) // (1 << 12) + 1)
+    cases.append(geo)
+    for w in cases:
+        for K in (8, 11, 12):
+            hs = codec.encode(w, layout=codec.make_layout(8, 64, K))
+            assert codec.validate(hs) == 0
+
+
 def test_encode_rejects_mismatched_codebook():
     w = synth.gaussian(10_000, 0.02, 1)
     cb = codec.build_codebook(synth.gaussian(10_000, 0.02, 2))

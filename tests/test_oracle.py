@@ -260,6 +260,28 @@ def test_entropy_bound(kind):
     assert H - 1e-12 <= Lbar < H + 1
 
 
+@pytest.mark.parametrize("config", ["matrix_4096", "llama3_8b_block", "heavy_tailed_block",
+                                    "llama31_70b_block"])
+def test_kraft_and_entropy_bound_on_workload_histograms(config):
+    """Pins P2 and P3 on the histograms of the four decode workloads (Sec. 2.1,
+    Huffman optimality): the code is a complete prefix code (Kraft sum 1,
+    exact in integers) and its mean length is within one bit of the
+    exponent entropy."""
+    w = {"matrix_4096": synth.matrix_4096,
+         "llama3_8b_block": lambda: synth.llama3_8b_block()[0],
+         "heavy_tailed_block": synth.heavy_tailed_block,
+         "llama31_70b_block": lambda: synth.llama31_70b_block()[0]}[config]()
+    counts = oracle.histogram(w)
+    assert int(counts.sum()) == w.size
+    del w
+    lengths = oracle.code_lengths(counts, 32)
+    assert kraft_scaled(lengths) == 1 << 32
+    assert lengths.max() <= 32 and all((lengths > 0) == (counts > 0))
+    H = entropy_bits(counts)
+    Lbar = cost(counts, lengths) / counts.sum()
+    assert H - 1e-12 <= Lbar < H + 1
+
+
 def test_histogram_definition():
     w = synth.special_values(3000)
     ref = np.zeros(256, np.uint64)
