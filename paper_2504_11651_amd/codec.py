@@ -432,6 +432,12 @@ def block_gemv(ds: DeviceStream, mats, xs, ys, workspace=None, stream=None):
     if workspace is None:
         workspace = torch.empty(max(gemv_workspace_bytes(ds, mats) // 4, 4), dtype=torch.float32,
                                 device=ds.device)
+        # the kernels run on `stream`: the caching allocator must not hand this
+        # memory out again before that stream has finished with it
+        s = torch.cuda.current_stream(ds.device) if stream is None else stream
+        if not hasattr(s, "cuda_stream"):
+            s = torch.cuda.ExternalStream(int(s), device=ds.device)
+        workspace.record_stream(s)
     _on_device(workspace, ds.device, "workspace")
     xp = (ctypes.c_void_p * len(xs))(*[x.data_ptr() for x in xs])
     yp = (ctypes.c_void_p * len(ys))(*[y.data_ptr() for y in ys])

@@ -262,7 +262,7 @@ int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *bloc
             if (pc < 1) return DF11_E_UNSUPPORTED;
             ls.per_cu = static_cast<uint32_t>(pc);
         }
-        if (di.shapes.size() >= kMaxShapes) di.shapes.clear();  // bounded lookup cost
+        if (di.shapes.size() >= kMaxShapes) di.shapes.erase(di.shapes.begin());  // oldest goes
         di.shapes.push_back(ls);
         found = &di.shapes.back();
     }

@@ -431,7 +431,7 @@ int choose_ranges(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens, uin
         e.cols[m] = mats[m].cols;
         e.ks_req[m] = ks_req[m];
     }
-    if (g_splits.size() >= kMaxSplits) g_splits.clear();  // bounded lookup cost
+    if (g_splits.size() >= kMaxSplits) g_splits.erase(g_splits.begin());  // oldest goes first
     g_splits.push_back(e);
     return DF11_OK;
 }

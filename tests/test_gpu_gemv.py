@@ -144,3 +144,26 @@ def test_random_streams_gemv(seed):
     ys2 = run_gemv(ds, mats, xs_h)
     for a, b in zip(ys, ys2):
         assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_gemv_on_a_side_stream_without_workspace():
+    """block_gemv on a stream other than torch's current one, with the
+    workspace left to the binding: the result matches the current-stream call
+    bit for bit, and memory allocated while the side stream still runs does
+    not disturb it."""
+    import torch
+    w, mats = make_stream([(48, 4096), (16, 2048)], 1234)
+    ds = codec.to_device(codec.encode(w), "cuda")
+    xs_h = [synth.activations(1, c, 1235, i) for i, (_, _, c) in enumerate(mats)]
+    ref = run_gemv(ds, mats, xs_h)
+    side = torch.cuda.Stream()
+    xs = [torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16).reshape(-1) for x in xs_h]
+    ys = [torch.full((r,), float("nan"), dtype=torch.float32, device="cuda") for _, r, _ in mats]
+    torch.cuda.synchronize()
+    for _ in range(3):
+        codec.block_gemv(ds, mats, xs, ys, stream=side)
+        junk = torch.full((1 << 20,), 7.0, device="cuda")  # reuses freed blocks if unprotected
+        del junk
+    side.synchronize()
+    for a, b in zip(ys, ref):
+        assert np.array_equal(a.cpu().numpy().view(np.uint32), b.view(np.uint32))
