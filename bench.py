@@ -20,6 +20,10 @@ the warm back-to-back mean are reported beside it.
 --workload llama3_8b_stack times the decode-then-products driver instead: 32
 blocks resident in compressed form, one step = decode one block into a reused
 workspace plus its 7 products at T activation rows.
+
+--workload lm_head_sweep decodes slices of an LM-head-shaped matrix (the first
+R rows of 128,256 x 4096, R = 1,024 .. 128,256, each its own stream) and times
+a pinned-host-to-device copy of the same BF16 bytes beside each decode.
 """
 from __future__ import annotations
 
@@ -185,6 +189,103 @@ def run_stack(args) -> int:
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = stack_cpu_baseline(hs0, w0, mats, [x1_h] * 6 + [x2_h], n)
     print(json.dumps(rec), flush=True)
+    return 0
+
+
+SWEEP_ROWS = (1024, 2048, 4096, 8192, 16384, 32768, 65536, 128256)
+
+
+def run_sweep(args) -> int:
+    """Matrix-size sweep on LM-head-shaped slices (the first R rows of a
+    128,256 x 4096 matrix, each slice its own stream): decode throughput per
+    size, and beside it a copy of the same BF16 bytes from pinned host memory
+    to the GPU.  The paper's decode-speed experiment compares the two across
+    matrix sizes; its premise is that decode throughput rises with size."""
+    import torch
+    from paper_2504_11651_amd import codec, synth
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream(dev)
+    t0 = time.perf_counter()
+    w_all = synth.lm_head()
+    t_gen = time.perf_counter() - t0
+    cols = synth.LM_HEAD_COLS
+    flush = torch.ones(1 << 28, dtype=torch.int32, device=dev)
+    pinned = torch.empty(w_all.size, dtype=torch.int16, pin_memory=True)
+    pinned.numpy()[:] = w_all.view(np.int16)
+    dst = torch.empty(w_all.size, dtype=torch.int16, device=dev)
+    rows_list = [r for r in SWEEP_ROWS if r <= synth.LM_HEAD_ROWS]
+    sweep, head, hs_small, w_small = [], None, None, None
+    for rows in rows_list:
+        w = w_all[:rows * cols]
+        n = w.size
+        hs = codec.encode(w)
+        assert codec.validate(hs) == 0
+        ds = codec.to_device(hs, dev)
+        out = torch.empty(n, dtype=torch.bfloat16, device=dev)
+        out.view(torch.int16).fill_(0x5555)
+        codec.decode_block(ds, out, stream=stream)
+        torch.cuda.synchronize()
+        exact = bool(torch.equal(out.view(torch.int16), dst[:n].copy_(pinned[:n])))
+        assert exact, f"{rows} rows: decode is not bit-exact"
+        fn = lambda: codec.decode_block(ds, out, stream=stream)
+        for _ in range(args.warmup):
+            fn()
+        settle(fn, stream, min(args.settle_ms, 150.0))
+        dec = cold_and_warm(fn, stream, args.steps, flush)["cold"]
+        # host-to-device copy of the same BF16 bytes from pinned memory, and of
+        # the compressed stream (what a compressed host-side copy would move)
+        h2d = []
+        for _ in range(max(5, min(args.steps, 20))):
+            s_ev, e_ev = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            s_ev.record(stream)
+            dst[:n].copy_(pinned[:n], non_blocking=True)
+            e_ev.record(stream)
+            e_ev.synchronize()
+            h2d.append(s_ev.elapsed_time(e_ev))
+        t_dec = float(np.median(dec))
+        t_h2d = float(np.median(h2d))
+        algo = hs.compressed_bytes + 2 * n
+        comp_h2d_ms = t_h2d * hs.compressed_bytes / (2.0 * n)
+        rec = {"rows": rows, "weights": n, "bit_exact": exact,
+               "decode_ms": round(t_dec, 5),
+               "decode_ms_min_max": [round(float(dec.min()), 5), round(float(dec.max()), 5)],
+               "decode_bf16_gbs": round(2.0 * n / (t_dec * 1e-3) / 1e9, 1),
+               "frac": round(algo / (t_dec * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+               "h2d_bf16_ms": round(t_h2d, 5),
+               "h2d_bf16_gbs": round(2.0 * n / (t_h2d * 1e-3) / 1e9, 2),
+               "decode_over_h2d": round(t_h2d / t_dec, 2),
+               "compressed_h2d_plus_decode_ms": round(comp_h2d_ms + t_dec, 5),
+               "bits_per_weight": round(8 + hs.sizes.total_bits / n, 4)}
+        sweep.append(rec)
+        print(f"# lm_head {rows} rows: decode {t_dec:.5f} ms ({rec['decode_bf16_gbs']} GB/s), "
+              f"h2d {t_h2d:.5f} ms, ratio {rec['decode_over_h2d']}", file=sys.stderr, flush=True)
+        if rows == rows_list[-1]:
+            head = (rec, algo, hs)
+        if rows == rows_list[0]:
+            hs_small, w_small = hs, w
+        del ds, out
+        torch.cuda.empty_cache()
+    del flush, dst
+    rec, algo, hs = head
+    n = rec["weights"]
+    line = {
+        "metric": METRIC, "value": rec["decode_bf16_gbs"], "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": rec["decode_ms"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+        "data": "synthetic",
+        "config": {"workload": "lm_head_sweep", "matrix": "128256 x 4096 LM head, N(0, 0.02^2)",
+                   "slices": "first R rows, each its own stream", "rows": rows_list,
+                   "timing": "decode: cold median per size; h2d: median copy from pinned host "
+                             "memory (torch pin_memory) of the same BF16 bytes"},
+        "roofline": {"bound": "hbm", "achieved": round(algo / (rec["decode_ms"] * 1e-3) / 1e9, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": rec["frac"], "traffic": None},
+        "sweep": sweep,
+        "max_decode_over_h2d": max(r["decode_over_h2d"] for r in sweep),
+        "host_s": {"generate": round(t_gen, 2)},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(hs_small, w_small, max_reps=2000)
+    print(json.dumps(line), flush=True)
     return 0
 
 
@@ -425,7 +526,8 @@ def main() -> int:
                     help="back-to-back launches before timing, in GPU milliseconds")
     ap.add_argument("--workload", default=HEADLINE,
                     help="llama31_70b_block (default), llama3_8b_block, heavy_tailed_block, "
-                         "matrix_4096, llama3_8b_stack (decode + 7 products per step)")
+                         "matrix_4096, llama3_8b_stack (decode + 7 products per step), "
+                         "lm_head_sweep (decode vs host-to-device copy across matrix sizes)")
     ap.add_argument("--tokens", type=int, default=64, help="activation rows (llama3_8b_stack)")
     ap.add_argument("--threads", type=int, default=None, help="threads per block T")
     ap.add_argument("--lut-bits", type=int, default=None)
@@ -447,6 +549,8 @@ def main() -> int:
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.workload == "llama3_8b_stack":
         return run_stack(args)
+    if args.workload == "lm_head_sweep":
+        return run_sweep(args)
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
     lay = codec.make_layout(8, args.threads, args.lut_bits)

@@ -120,6 +120,19 @@ def llama31_70b_block(block: int = 0):
     return _block(LLAMA31_70B_BLOCK, 4, block, 0.005, 0.03)
 
 
+LM_HEAD_ROWS, LM_HEAD_COLS = 128_256, 4096  # Llama-3.1-8B vocabulary x hidden size
+
+
+def lm_head(rows: int = LM_HEAD_ROWS, cols: int = LM_HEAD_COLS, seed: int = 0) -> np.ndarray:
+    """The first ``rows`` rows of an LM-head-shaped matrix (128,256 x 4096,
+    row-major [vocab, hidden]) ~ N(0, 0.02^2).  Every piece is seeded on its
+    own, so a prefix of rows is the same whatever ``rows`` is: the slices of
+    the size sweep are prefixes of one matrix."""
+    out = np.empty(rows * cols, np.uint16)
+    _fill_pieces(out, (7, seed, cols), _normal(0.02))
+    return out
+
+
 def llama3_8b_stack_block(i: int):
     """Block i of the 32-block Llama-3-8B-shaped stack (block seeds (5, i))."""
     return _block(LLAMA3_8B_BLOCK, 5, i, 0.008, 0.04)
