@@ -497,6 +497,40 @@ def measure_decode(name: str, w: np.ndarray, lay, args, dev, flush, full: bool) 
     return rec
 
 
+def measure_hlut(name: str, w: np.ndarray, T: int, args, dev, flush) -> dict:
+    """The paper's own kernel design (hierarchical 8-bit tables, two-phase
+    re-decode, per-element sign/mantissa gather, LDS write buffer) on the same
+    workload, in a stream with T threads per block, same timing protocol."""
+    import torch
+    from paper_2504_11651_amd import codec
+    hs = codec.encode(w, layout=codec.make_layout(8, T, 11))
+    ds = codec.to_device(hs, dev)
+    hl = codec.DeviceHlut(hs, dev)
+    n = w.size
+    out = torch.empty(n, dtype=torch.bfloat16, device=dev)
+    out.view(torch.int16).fill_(0x5555)
+    stream = torch.cuda.current_stream(dev)
+    codec.decode_block_hlut(ds, hl, out, stream=stream)
+    ref = torch.from_numpy(w.view(np.int16)).to(dev)
+    torch.cuda.synchronize()
+    exact = bool(torch.equal(out.view(torch.int16), ref))
+    assert exact, f"{name}: the paper's kernel is not bit-exact"
+    del ref
+    fn = lambda: codec.decode_block_hlut(ds, hl, out, stream=stream)
+    settle(fn, stream, min(args.settle_ms, 200.0))
+    cold = cold_and_warm(fn, stream, args.steps, flush)["cold"]
+    med = float(np.median(cold))
+    algo = hs.compressed_bytes - int(hs.sizes.table_bytes) + hl.tables.numel() + 2 * n
+    del ds, out, hl
+    torch.cuda.empty_cache()
+    return {"threads_per_block": T, "bit_exact": exact, "luts": int(codec.build_hlut_tables(
+                hs.codebook)[1]),
+            "ms": {"cold_median": round(med, 5), "cold_min": round(float(cold.min()), 5),
+                   "cold_max": round(float(cold.max()), 5)},
+            "bf16_gbs": round(2.0 * n / (med * 1e-3) / 1e9, 2),
+            "frac": round(algo / (med * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+
+
 def device_copy_gbs(dev, stream) -> float:
     """Context: what a plain device-to-device copy (read + write, no decode)
     sustains, 512 MiB each way (twice the last-level cache), event timed."""
@@ -533,6 +567,9 @@ def main() -> int:
     ap.add_argument("--lut-bits", type=int, default=None)
     ap.add_argument("--no-per-config", action="store_true",
                     help="time only --workload, not the other block configurations")
+    ap.add_argument("--no-ablation", action="store_true",
+                    help="skip the paper's own kernel design (hierarchical tables, two-phase "
+                         "re-decode) timed on the same blocks")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib", action="store_true",
                     help="also run a plain device copy of known size (PMC calibration)")
@@ -572,6 +609,15 @@ def main() -> int:
     hs = head.pop("_hs")
     timed_region_s = head.pop("timed_region_s")
     launch = head.pop("launch")
+    ablation = {}
+    if not args.no_ablation:
+        ablation[args.workload] = [measure_hlut(args.workload, w, T, args, dev, flush)
+                                   for T in (256, 1024)]
+        if "llama3_8b_block" in per_config:
+            w2 = workload("llama3_8b_block")
+            ablation["llama3_8b_block"] = [measure_hlut("llama3_8b_block", w2, T, args, dev, flush)
+                                           for T in (256, 1024)]
+            del w2
     del flush
     torch.cuda.empty_cache()
 
@@ -632,6 +678,8 @@ def main() -> int:
     }
     if per_config:
         rec["per_config"] = per_config
+    if ablation:
+        rec["ablation_paper_kernel"] = ablation
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(hs, w)
     print(json.dumps(rec), flush=True)

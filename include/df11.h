@@ -272,6 +272,42 @@ int df11_block_gemv(const df11_stream *dev, const df11_matrix *mats, uint32_t n_
                     const uint16_t *const *x, float *const *y, void *workspace,
                     uint64_t workspace_bytes, hipStream_t stream);
 
+/* ---- The paper's own decoder, as an ablation (Sec. 2.3.1 hierarchical
+ * lookup tables; Sec. 2.3.2 and Algorithm 1 two-phase kernel; appendix on
+ * compact lookup tables).  It decodes the same streams as df11_decode_block
+ * with the paper's tables and kernel design, so the two designs can be
+ * compared on the same hardware and data.
+ *
+ * df11_build_hlut_tables: the Huffman tree of cb cut into subtrees of height
+ * level_bits (8 for the decoder; 1..8 accepted), one table of 2^level_bits
+ * exponent bytes per subtree, LUT_1 for the root; an entry is the exponent
+ * whose code is a prefix of the bits read so far, or a pointer v in 240..255
+ * to LUT_(257-v) which decodes the next level_bits bits.  Writes LUT_1 ..
+ * LUT_k in creation order (breadth first), then CodeLengths[256] (the code
+ * length of every exponent), (k << level_bits) + 256 bytes in all; *num_luts
+ * = k.  Host.  DF11_E_UNSUPPORTED when cb uses an exponent of 240 or more
+ * (the paper's format reserves them as pointers) or needs more than
+ * DF11_HLUT_MAX_LUTS tables; DF11_E_BUFFER_TOO_SMALL (with *num_luts set)
+ * when table_cap is short. */
+#define DF11_HLUT_MAX_LUTS 17
+#define DF11_HLUT_MAX_BYTES ((DF11_HLUT_MAX_LUTS + 1) * 256)
+int df11_build_hlut_tables(const df11_codebook *cb, uint32_t level_bits, uint8_t *tables,
+                           uint64_t table_cap, uint32_t *num_luts);
+
+/* df11_decode_block_hlut: decompress stream dev into out (device, 2*n_elems
+ * bytes, 16-byte aligned) with the paper's kernel: one workgroup of T =
+ * dev->layout.threads_per_block threads per block, tables and the block's
+ * EncodedExponent bytes staged in LDS, phase 1 decodes one code per step
+ * through the table hierarchy and counts, a Blelloch scan gives each thread
+ * its output position, phase 2 decodes again and gathers each element's
+ * sign/mantissa byte into an LDS write buffer, then coalesced stores.  luts:
+ * device copy of df11_build_hlut_tables's output at level_bits 8 (16-byte
+ * aligned, (num_luts + 1) * 256 bytes), num_luts its k (1..17).  dev->tables
+ * is not used.  Enqueued on `stream`; DF11_E_INVALID_ARG / DF11_E_UNSUPPORTED
+ * as df11_decode_block. */
+int df11_decode_block_hlut(const df11_stream *dev, const uint8_t *luts, uint32_t num_luts,
+                           uint16_t *out, hipStream_t stream);
+
 /* Static description of a status code. */
 const char *df11_strerror(int status);
 

@@ -9,7 +9,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libdf11.so")
-SOURCES = ["df11_host.cpp", "df11_tables.cpp", "df11_decode.hip", "df11_gemm.hip", "df11_gemv.hip"]
+SOURCES = ["df11_host.cpp", "df11_tables.cpp", "df11_decode.hip", "df11_gemm.hip", "df11_gemv.hip",
+           "df11_hlut_host.cpp", "df11_hlut.hip"]
 
 HIP_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

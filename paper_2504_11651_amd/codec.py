@@ -28,6 +28,7 @@ EXPORTS = (
     "df11_build_tables", "df11_validate", "df11_decode_block", "df11_decode_launch_shape",
     "df11_gemm_workspace_bytes", "df11_block_gemm", "df11_block_forward",
     "df11_block_forward_noalloc", "df11_gemv_workspace_bytes", "df11_block_gemv", "df11_strerror",
+    "df11_build_hlut_tables", "df11_decode_block_hlut",
 )
 
 MAX_MATRICES = 8  # DF11_MAX_MATRICES
@@ -123,6 +124,8 @@ def lib():
                                        ctypes.c_uint32, P(vp), vp],
         "df11_gemv_workspace_bytes": [P(Stream), P(Matrix), ctypes.c_uint32, P(u64)],
         "df11_block_gemv": [P(Stream), P(Matrix), ctypes.c_uint32, P(vp), P(vp), vp, u64, vp],
+        "df11_build_hlut_tables": [P(Codebook), ctypes.c_uint32, vp, u64, P(ctypes.c_uint32)],
+        "df11_decode_block_hlut": [P(Stream), vp, ctypes.c_uint32, vp, vp],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -447,3 +450,45 @@ def block_gemv(ds: DeviceStream, mats, xs, ys, workspace=None, stream=None):
                                  ctypes.c_void_p(_handle(stream, ds.device))),
            "df11_block_gemv")
     return ys
+
+
+# ------------------------------------ the paper's decoder (ablation)
+HLUT_MAX_BYTES = 18 * 256  # DF11_HLUT_MAX_BYTES
+
+
+def build_hlut_tables(cb: Codebook, level_bits: int = 8):
+    """(tables, k): the paper's hierarchical lookup tables LUT_1..LUT_k
+    (2**level_bits bytes each) followed by CodeLengths[256]."""
+    k = ctypes.c_uint32()
+    buf = np.zeros(HLUT_MAX_BYTES if level_bits == 8 else (17 << level_bits) + 256, np.uint8)
+    rc = lib().df11_build_hlut_tables(ctypes.byref(cb), level_bits, _ptr(buf), buf.size,
+                                      ctypes.byref(k))
+    _check(rc, "df11_build_hlut_tables")
+    return buf[:(int(k.value) << level_bits) + 256].copy(), int(k.value)
+
+
+class DeviceHlut:
+    """The paper's tables for one stream, in device memory."""
+
+    def __init__(self, hs: HostStream, device="cuda"):
+        import torch
+        tabs, self.k = build_hlut_tables(hs.codebook, 8)
+        self.tables = torch.from_numpy(tabs).to(torch.device(device))
+
+
+def decode_block_hlut(ds: DeviceStream, hl: DeviceHlut, out=None, stream=None):
+    """Decode ``ds`` with the paper's kernel and tables ``hl`` into ``out``."""
+    import torch
+    n = ds.n_elems
+    if out is None:
+        out = torch.empty(n, dtype=torch.bfloat16, device=ds.device)
+    if out.numel() < n or out.element_size() != 2 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous 2-byte tensor with n_elems elements")
+    _on_device(out, ds.device, "out")
+    _on_device(hl.tables, ds.device, "tables")
+    _check(lib().df11_decode_block_hlut(ctypes.byref(ds.struct()),
+                                        ctypes.c_void_p(hl.tables.data_ptr()), hl.k,
+                                        ctypes.c_void_p(out.data_ptr()),
+                                        ctypes.c_void_p(_handle(stream, ds.device))),
+           "df11_decode_block_hlut")
+    return out
