@@ -87,10 +87,13 @@ def run_stack(args) -> int:
             w0, hs0 = w, hs
     t_prep = time.perf_counter() - t0
     T = args.tokens
-    x1_h = synth.activations(T, 4096, 5, 0, 1)
-    x2_h = synth.activations(T, 14336, 5, 0, 2)
-    x1 = torch.from_numpy(x1_h.view(np.int16)).to(dev)
-    x2 = torch.from_numpy(x2_h.view(np.int16)).to(dev)
+    x1_h = synth.activations(64, 4096, 5, 0, 1)
+    x2_h = synth.activations(64, 14336, 5, 0, 2)
+    x1_full = torch.from_numpy(x1_h.view(np.int16)).to(dev).view(torch.bfloat16)
+    x2_full = torch.from_numpy(x2_h.view(np.int16)).to(dev).view(torch.bfloat16)
+    x1_h, x2_h = x1_h[:T], x2_h[:T]
+    x1 = x1_full.view(torch.int16)[:T]
+    x2 = x2_full.view(torch.int16)[:T]
     xs = [x1.view(torch.bfloat16)] * 6 + [x2.view(torch.bfloat16)]
     ys = [torch.empty((T, r), dtype=torch.float32, device=dev) for _, r, _ in mats]
     ws = torch.empty(max(codec.gemm_workspace_bytes(mats, T) // 4, 1), dtype=torch.float32,
@@ -152,6 +155,29 @@ def run_stack(args) -> int:
     _, dec_ms = timed(dec, args.steps)
     _, gemm_ms = timed(gemm, args.steps)
 
+    # latency breakdown over token counts (decode is the same work at every t)
+    breakdown = []
+    if not args.no_sweep:
+        for t in STACK_TOKENS:
+            xs_t = [x1_full[:t]] * 6 + [x2_full[:t]]
+            ys_t = [torch.empty((t, r), dtype=torch.float32, device=dev) for _, r, _ in mats]
+            ws_t = torch.empty(max(codec.gemm_workspace_bytes(mats, t) // 4, 1),
+                               dtype=torch.float32, device=dev)
+            st_fn = lambda i: codec.block_forward(streams[i % blocks], work, mats, xs_t, ys_t,
+                                                  ws_t, stream=stream)
+            pr_fn = lambda i: codec.block_gemm(work, mats, xs_t, ys_t, ws_t, stream=stream)
+            _, st_ms = timed(st_fn, args.steps)
+            _, pr_ms = timed(pr_fn, args.steps)
+            pb = 2 * n + 2 * t * (6 * 4096 + 14336) + 4 * t * sum(r for _, r, _ in mats)
+            breakdown.append({"tokens": t, "step_ms": round(st_ms, 5), "decode_ms": round(dec_ms, 5),
+                              "products_ms": round(pr_ms, 5),
+                              "decode_share": round(dec_ms / st_ms, 3),
+                              "products_gbs": round(pb / (pr_ms * 1e-3) / 1e9, 1),
+                              "tokens_per_s_per_block": round(t / (st_ms * 1e-3), 1)})
+            del xs_t, ys_t, ws_t
+    overlap = overlapped_schedule(codec, streams, mats, x1_full, x2_full, n, args, dev) \
+        if not args.no_sweep else None
+
     mean_comp = mean_comp_bytes()
     x_bytes = 2 * T * (6 * 4096 + 14336)
     y_bytes = 4 * T * sum(r for _, r, _ in mats)
@@ -186,6 +212,10 @@ def run_stack(args) -> int:
     }
     if fused is not None:
         rec["fused_decode_gemv"] = fused
+    if breakdown:
+        rec["latency_breakdown"] = breakdown
+    if overlap is not None:
+        rec["overlapped_schedule"] = overlap
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = stack_cpu_baseline(hs0, w0, mats, [x1_h] * 6 + [x2_h], n)
     print(json.dumps(rec), flush=True)
@@ -287,6 +317,75 @@ def run_sweep(args) -> int:
         line["cpu_baseline"] = cpu_baseline(hs_small, w_small, max_reps=2000)
     print(json.dumps(line), flush=True)
     return 0
+
+
+STACK_TOKENS = (1, 2, 4, 8, 16, 32, 64)
+
+
+def overlapped_schedule(codec, streams, mats, x1_full, x2_full, n, args, dev) -> dict:
+    """Decode of block i+1 on a second stream, into a second BF16 workspace,
+    while block i's products run (events order each workspace's reuse),
+    against the sequential step on one stream.  Outputs of the last block must
+    be bit-identical to the sequential run's."""
+    import torch
+    blocks = len(streams)
+    res = {}
+    dec_s = torch.cuda.Stream(dev)
+    prod_s = torch.cuda.current_stream(dev)
+    for t in (1, 64):
+        xs = [x1_full[:t]] * 6 + [x2_full[:t]]
+        ws = torch.empty(max(codec.gemm_workspace_bytes(mats, t) // 4, 1), dtype=torch.float32,
+                         device=dev)
+        work = [torch.empty(n, dtype=torch.bfloat16, device=dev) for _ in range(2)]
+        ys = [torch.empty((t, r), dtype=torch.float32, device=dev) for _, r, _ in mats]
+        ys_seq = [torch.empty_like(y) for y in ys]
+        steps = max(args.steps, 2 * blocks)
+
+        def sequential():
+            for i in range(steps):
+                codec.block_forward(streams[i % blocks], work[0], mats, xs, ys_seq, ws,
+                                    stream=prod_s)
+
+        def overlapped():
+            decoded = [torch.cuda.Event() for _ in range(2)]
+            consumed = [torch.cuda.Event() for _ in range(2)]
+            codec.decode_block(streams[0], work[0], stream=dec_s)
+            decoded[0].record(dec_s)
+            for i in range(steps):
+                cur, nxt = i % 2, (i + 1) % 2
+                if i + 1 < steps:
+                    if i >= 1:
+                        dec_s.wait_event(consumed[nxt])
+                    codec.decode_block(streams[(i + 1) % blocks], work[nxt], stream=dec_s)
+                    decoded[nxt].record(dec_s)
+                prod_s.wait_event(decoded[cur])
+                codec.block_gemm(work[cur], mats, xs, ys, ws, stream=prod_s)
+                consumed[cur].record(prod_s)
+
+        out = {"sequential": [], "overlapped": []}
+        for _ in range(3):  # alternate the two schedules, each after its own settle
+            for name, fn in (("sequential", sequential), ("overlapped", overlapped)):
+                t_end = time.perf_counter() + args.settle_ms * 1e-3
+                while time.perf_counter() < t_end:
+                    fn()
+                    torch.cuda.synchronize()
+                s_ev = torch.cuda.Event(enable_timing=True)
+                e_ev = torch.cuda.Event(enable_timing=True)
+                s_ev.record(prod_s)
+                dec_s.wait_event(s_ev)  # the decode stream starts inside the timed region too
+                fn()
+                e_ev.record(prod_s)
+                torch.cuda.synchronize()
+                out[name].append(s_ev.elapsed_time(e_ev) / steps)
+        out = {k: float(np.median(v)) for k, v in out.items()}
+        same = all(torch.equal(a.view(torch.int32), b.view(torch.int32)) for a, b in zip(ys, ys_seq))
+        assert same, "overlapped schedule differs from the sequential one"
+        res[f"tokens_{t}"] = {"sequential_ms_per_step": round(out["sequential"], 5),
+                              "overlapped_ms_per_step": round(out["overlapped"], 5),
+                              "bit_identical": same}
+        del work, ws, ys, ys_seq
+        torch.cuda.empty_cache()
+    return res
 
 
 def stack_cpu_baseline(hs, w, mats, xs, n) -> dict:
@@ -567,6 +666,8 @@ def main() -> int:
     ap.add_argument("--lut-bits", type=int, default=None)
     ap.add_argument("--no-per-config", action="store_true",
                     help="time only --workload, not the other block configurations")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="llama3_8b_stack: skip the token sweep and the overlapped schedule")
     ap.add_argument("--no-ablation", action="store_true",
                     help="skip the paper's own kernel design (hierarchical tables, two-phase "
                          "re-decode) timed on the same blocks")
