@@ -439,7 +439,7 @@ def profiled_traffic(workload_name: str, lay) -> float | None:
             h.update(f.read())
     want = {"workload": workload_name, "source_sha256": h.hexdigest(),
             "layout": f"{lay.bytes_per_thread},{lay.threads_per_block},{lay.lut_bits}"}
-    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*_counters.md"))):
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "df11_decode_*.md"))):
         kv = {}
         with open(path) as f:
             for line in f:
