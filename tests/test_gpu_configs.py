@@ -176,3 +176,31 @@ def test_llama3_8b_stack_decode_then_gemm(stack_streams, tokens):
             mag = oracle.linear(x & 0x7FFF, wm & 0x7FFF)
             assert np.all(np.abs(y - ref) <= c * 2.0 ** -23 * mag + 1e-30), f"block {i} matrix {m}"
     print(f"tokens={tokens}: worst relative Frobenius error vs fp32 reference {worst:.3g}")
+
+
+@pytest.mark.parametrize("tokens", [1, 64])
+def test_llama3_8b_stack_block0_every_output(stack_streams, tokens):
+    """Every output of one full stack block (block 0, all 7 matrices) against
+    the oracle's float64 product, within the fp32-accumulation bound
+    k * 2^-23 * sum |x w|, at 1 and 64 tokens (the split-k layouts the
+    products use at both token counts)."""
+    import torch
+    mats, n = stack_mats()
+    w, _ = synth.llama3_8b_stack_block(0)
+    xs_h = stack_activations(0, tokens)
+    xs = [torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16) for x in xs_h]
+    ys = [torch.full((tokens, r), float("nan"), dtype=torch.float32, device="cuda")
+          for _, r, _ in mats]
+    work = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(max(codec.gemm_workspace_bytes(mats, tokens) // 4, 1), dtype=torch.float32,
+                     device="cuda")
+    codec.block_forward(stack_streams[0], work, mats, xs, ys, ws)
+    torch.cuda.synchronize()
+    for m, ((off, r, c), x, y) in enumerate(zip(mats, xs_h, ys)):
+        wm = w[off:off + r * c].reshape(r, c)
+        got = y.cpu().numpy().astype(np.float64)
+        assert np.all(np.isfinite(got)), f"matrix {m}: unwritten outputs"
+        ref = oracle.linear(x, wm)
+        mag = oracle.linear(x & 0x7FFF, wm & 0x7FFF)
+        bad = np.abs(got - ref) > c * 2.0 ** -23 * mag + 1e-30
+        assert not bad.any(), f"matrix {m}: {int(bad.sum())} of {got.size} outputs outside the bound"

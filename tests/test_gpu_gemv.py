@@ -97,9 +97,9 @@ def test_block_gemv_matches_oracle_and_driver(name):
         assert np.all(np.abs(a - b.cpu().numpy()[0]) <= 2 * c * 2.0 ** -23 * mag + 1e-30)
 
 
-def test_block_gemv_llama3_8b_block_sampled():
-    """Full Llama-3-8B-shaped block: sampled rows against the oracle, all rows
-    against decode-then-products."""
+def test_block_gemv_llama3_8b_block_every_output():
+    """Full Llama-3-8B-shaped block: every output against the oracle's float64
+    product, and against decode-then-products."""
     import torch
     w, offs = synth.llama3_8b_block()
     mats = [(off, r, c) for off, r, c, _ in offs.values()]
@@ -113,14 +113,12 @@ def test_block_gemv_llama3_8b_block_sampled():
                       device="cuda")
     codec.block_forward(ds, work, mats, xs, yd, wsp)
     torch.cuda.synchronize()
-    rng = np.random.default_rng(0)
     for (off, r, c), y, yb, x in zip(mats, ys, yd, xs_h):
         assert np.all(np.isfinite(y))
-        rows = np.sort(rng.choice(r, 48, replace=False))
-        wm = w[off:off + r * c].reshape(r, c)[rows]
+        wm = w[off:off + r * c].reshape(r, c)
         ref = oracle.linear(x, wm)[0]
         mag = oracle.linear(x & 0x7FFF, wm & 0x7FFF)[0]
-        assert np.all(np.abs(y[rows].astype(np.float64) - ref) <= c * 2.0 ** -23 * mag + 1e-30)
+        assert np.all(np.abs(y.astype(np.float64) - ref) <= c * 2.0 ** -23 * mag + 1e-30)
         yb = yb.cpu().numpy()[0]
         rel = np.linalg.norm(y - yb) / np.linalg.norm(yb)
         assert rel <= 1e-5, rel
