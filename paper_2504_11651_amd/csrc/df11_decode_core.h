@@ -133,8 +133,13 @@ struct ChunkWords {
 
 __device__ __forceinline__ ChunkWords load_chunk(const DecodeArgs &a, uint32_t b, uint32_t c) {
     ChunkWords r;
-    r.bp0 = a.block_pos[b];
-    r.bp1 = a.block_pos[b + 1];
+    // BlockOutputPos is read-only for the whole launch and its index is
+    // uniform: through the constant address space these are scalar loads,
+    // which keep the vector memory path for the streams
+    const __attribute__((address_space(4))) uint32_t *bp =
+        (const __attribute__((address_space(4))) uint32_t *)a.block_pos;
+    r.bp0 = bp[b];
+    r.bp1 = bp[b + 1];
     const uint2 own = *reinterpret_cast<const uint2 *>(a.exp + 8ull * c);
     r.x = own.x;
     r.y = own.y;
