@@ -45,7 +45,8 @@ constexpr uint32_t kKTargetFew = 1024;
 constexpr uint32_t kKTargetMany = 4096;
 constexpr uint32_t kFewTokens = 32;
 constexpr uint32_t kSlabMinTokens = 4;  // fewer tokens: activations straight from memory
-constexpr uint32_t kWaves = 4;       // waves per workgroup
+constexpr uint32_t kWaves = 4;       // waves per workgroup, up to 3 tokens
+constexpr uint32_t kSlabWaves = 4;   // waves per workgroup sharing one activation slab
 constexpr uint32_t kMax = DF11_MAX_MATRICES;
 
 struct GemmArgs {
@@ -193,7 +194,7 @@ __global__ __launch_bounds__(64 * kWaves) void gemm_tiles_kernel(GemmArgs a) {
     write_tile<1>(a, m, rb, s, j, g, acc);
 }
 
-// Four or more tokens: a workgroup of kWaves waves covers 16*kWaves features
+// Four or more tokens: a workgroup of kSlabWaves waves covers 16*kSlabWaves features
 // over one k range and stages the activations of each 256-k slab in LDS once
 // for all its waves (rows padded by 16 bytes so the 16 lanes of one read
 // pass hit distinct banks).  Weights still stream straight into registers.
@@ -203,7 +204,7 @@ constexpr uint32_t kSlabStride = kSlabK * 2 + 16;   // bytes per token row in LD
 // (4 waves per SIMD: the accumulators then stay in VGPRs, which the compiler
 // otherwise spills to AGPRs at 3 waves per SIMD)
 template <uint32_t MT>
-__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(4))) void
+__global__ __launch_bounds__(64 * kSlabWaves) __attribute__((amdgpu_waves_per_eu(4))) void
 gemm_slab_kernel(GemmArgs a) {
     __shared__ __attribute__((aligned(16))) uint8_t slab[16 * MT * kSlabStride];
     const uint32_t tid = threadIdx.x;
@@ -217,7 +218,7 @@ gemm_slab_kernel(GemmArgs a) {
     const uint32_t s = local - rbw * m.ksplit;
     const uint32_t k0 = s * m.kchunk;
     const uint32_t k1 = umin(m.cols, k0 + m.kchunk);
-    const uint32_t rb = rbw * kWaves + wave;       // this wave's 16-feature tile
+    const uint32_t rb = rbw * kSlabWaves + wave;       // this wave's 16-feature tile
     const bool active = rb * kTileRows < m.rows;   // uniform
 
     const uint32_t j = lane & 15u;
@@ -225,17 +226,17 @@ gemm_slab_kernel(GemmArgs a) {
     const uint16_t *wrow =
         a.w + m.w_off + static_cast<uint64_t>(active ? rb * kTileRows + j : 0u) * m.cols + 8u * g;
 
-    // slab loading: 16-byte piece q = tid + 64*kWaves*i covers token
+    // slab loading: 16-byte piece q = tid + 64*kSlabWaves*i covers token
     // q / kRowPieces, k offset 8 * (q % kRowPieces) of the slab
     constexpr uint32_t kRowPieces = kSlabK / 8u;
     constexpr uint32_t kPieces = 16u * MT * kRowPieces;
-    constexpr uint32_t kPer = kPieces / (64u * kWaves);
-    static_assert(kPieces % (64u * kWaves) == 0, "whole pieces per thread");
+    constexpr uint32_t kPer = kPieces / (64u * kSlabWaves);
+    static_assert(kPieces % (64u * kSlabWaves) == 0, "whole pieces per thread");
     uint4 xr[kPer];
     auto load_slab = [&](uint32_t k) {
 #pragma unroll
         for (uint32_t i = 0; i < kPer; ++i) {
-            const uint32_t q = tid + 64u * kWaves * i;
+            const uint32_t q = tid + 64u * kSlabWaves * i;
             const uint32_t t = q / kRowPieces, kk = k + 8u * (q % kRowPieces);
             const bool ok = t < a.tokens && kk < k1;
             const uint4 v = load16(m.x + static_cast<uint64_t>(ok ? t : 0u) * m.cols + (ok ? kk : k0));
@@ -245,7 +246,7 @@ gemm_slab_kernel(GemmArgs a) {
     auto store_slab = [&]() {
 #pragma unroll
         for (uint32_t i = 0; i < kPer; ++i) {
-            const uint32_t q = tid + 64u * kWaves * i;
+            const uint32_t q = tid + 64u * kSlabWaves * i;
             *reinterpret_cast<uint4 *>(slab + (q / kRowPieces) * kSlabStride + 16u * (q % kRowPieces)) =
                 xr[i];
         }
@@ -357,8 +358,8 @@ uint64_t split_cost(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens, u
         uint32_t ks, kc;
         split_into(mats[m].cols, ks_req[m], &ks, &kc);
         const uint32_t rows = mats[m].rows, cols = mats[m].cols;
-        for (uint32_t r0 = 0; r0 < rows; r0 += kTileRows * kWaves) {
-            const uint64_t nr = rows - r0 < kTileRows * kWaves ? rows - r0 : kTileRows * kWaves;
+        for (uint32_t r0 = 0; r0 < rows; r0 += kTileRows * kSlabWaves) {
+            const uint64_t nr = rows - r0 < kTileRows * kSlabWaves ? rows - r0 : kTileRows * kSlabWaves;
             for (uint32_t s = 0; s < ks; ++s) {
                 const uint64_t len = cols - s * kc < kc ? cols - s * kc : kc;
                 load[wg++ % cus] += 2 * nr * len + (ks > 1 ? 4 * nr * tokens : 0);
@@ -412,7 +413,7 @@ int choose_ranges(const df11_matrix *mats, uint32_t n_mats, uint32_t tokens, uin
             trial[m] = base[m] << ((mask >> m) & 1u);
             uint32_t ks, kc;
             split_into(mats[m].cols, trial[m], &ks, &kc);
-            wg += uint64_t{(mats[m].rows + kTileRows * kWaves - 1) / (kTileRows * kWaves)} * ks;
+            wg += uint64_t{(mats[m].rows + kTileRows * kSlabWaves - 1) / (kTileRows * kSlabWaves)} * ks;
         }
         const uint64_t c = split_cost(mats, n_mats, tokens, static_cast<uint32_t>(cus), trial, load);
         if (c < best || (c == best && wg < best_wg)) {
@@ -509,7 +510,7 @@ int plan(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats, u
         g.y[m] = r.y[m] = y[m];
         r.out_start[m] = static_cast<uint32_t>(outs);
         tiles += static_cast<uint64_t>(d.rows / kTileRows) * ks;
-        wgs += static_cast<uint64_t>((d.rows + kTileRows * kWaves - 1) / (kTileRows * kWaves)) * ks;
+        wgs += static_cast<uint64_t>((d.rows + kTileRows * kSlabWaves - 1) / (kTileRows * kSlabWaves)) * ks;
         if (ks > 1) {
             part += static_cast<uint64_t>(d.rows) * ks * tokens;
             outs += static_cast<uint64_t>(d.rows) * tokens;
@@ -531,18 +532,18 @@ int plan(const uint16_t *weights, uint64_t n_weights, const df11_matrix *mats, u
 
 int launch(const GemmArgs &g, const ReduceArgs &r, hipStream_t stream) {
     const uint32_t mt = (g.tokens + 15) / 16;
-    const dim3 block(64 * kWaves);
+    const dim3 block(64 * kWaves), slab_block(64 * kSlabWaves);
     const dim3 grid_tiles((g.num_tiles + kWaves - 1) / kWaves), grid_wg(g.num_wg);
     switch (mt) {
     case 1:
         if (g.tokens < kSlabMinTokens)
             hipLaunchKernelGGL(gemm_tiles_kernel, grid_tiles, block, 0, stream, g);
         else
-            hipLaunchKernelGGL(gemm_slab_kernel<1>, grid_wg, block, 0, stream, g);
+            hipLaunchKernelGGL(gemm_slab_kernel<1>, grid_wg, slab_block, 0, stream, g);
         break;
-    case 2: hipLaunchKernelGGL(gemm_slab_kernel<2>, grid_wg, block, 0, stream, g); break;
-    case 3: hipLaunchKernelGGL(gemm_slab_kernel<3>, grid_wg, block, 0, stream, g); break;
-    default: hipLaunchKernelGGL(gemm_slab_kernel<4>, grid_wg, block, 0, stream, g); break;
+    case 2: hipLaunchKernelGGL(gemm_slab_kernel<2>, grid_wg, slab_block, 0, stream, g); break;
+    case 3: hipLaunchKernelGGL(gemm_slab_kernel<3>, grid_wg, slab_block, 0, stream, g); break;
+    default: hipLaunchKernelGGL(gemm_slab_kernel<4>, grid_wg, slab_block, 0, stream, g); break;
     }
     if (hipGetLastError() != hipSuccess) return DF11_E_HIP;
     if (r.total) {
