@@ -216,6 +216,8 @@ def run_stack(args) -> int:
         rec["latency_breakdown"] = breakdown
     if overlap is not None:
         rec["overlapped_schedule"] = overlap
+    if args.calib:
+        calib_copies(dev)
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = stack_cpu_baseline(hs0, w0, mats, [x1_h] * 6 + [x2_h], n)
     print(json.dumps(rec), flush=True)
@@ -630,6 +632,18 @@ def measure_hlut(name: str, w: np.ndarray, T: int, args, dev, flush) -> dict:
             "frac": round(algo / (med * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
 
 
+def calib_copies(dev) -> None:
+    """Five plain 512 MiB device copies: their FETCH_SIZE / WRITE_SIZE
+    counters scale the kernels' counters to bytes."""
+    import torch
+    src = torch.empty(1 << 29, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+
+
 def device_copy_gbs(dev, stream) -> float:
     """Context: what a plain device-to-device copy (read + write, no decode)
     sustains, 512 MiB each way (twice the last-level cache), event timed."""
@@ -723,13 +737,7 @@ def main() -> int:
     torch.cuda.empty_cache()
 
     if args.calib:
-        # plain copy kernel of known size for scaling FETCH_SIZE / WRITE_SIZE counters
-        src = torch.empty(1 << 29, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(5):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        calib_copies(dev)
     copy_gbs = device_copy_gbs(dev, stream)
 
     n = w.size
