@@ -393,6 +393,36 @@ def test_layout_sizes():
                    "gap_bytes": 4 * (-(-5 * 65 // 32) + 2)}
 
 
+@pytest.mark.parametrize("n_bytes,threads", [(4, 64), (8, 64), (8, 256), (16, 128), (8, 1024)])
+def test_layout_by_enumeration(n_bytes, threads):
+    """Chunk and block counts by walking the stream (a chunk exists while its
+    first bit lies before total_bits; a block while its first chunk exists),
+    and the padding the readers need: every chunk can be read with the 4
+    bytes that follow it (Algorithm 1 reads 4 bytes past a position), and
+    the two 32-bit Gaps words holding the last slot (B*T) are inside the
+    buffer (Sec. 2.3.2, readings S5-S8)."""
+    rng = np.random.default_rng(n_bytes * threads)
+    cb = 8 * n_bytes
+    sizes = [0, 1, cb - 1, cb, cb + 1, cb * threads - 1, cb * threads, cb * threads + 1]
+    sizes += rng.integers(0, 40 * cb * threads, size=30).tolist()
+    for total_bits in sizes:
+        lay = oracle.layout(int(total_bits), n_bytes, threads)
+        chunks = 0
+        while cb * chunks < total_bits:
+            chunks += 1
+        blocks = 0
+        while threads * blocks < chunks:
+            blocks += 1
+        assert lay["num_chunks"] == chunks and lay["num_blocks"] == blocks, total_bits
+        # every chunk of every block, plus the 4 bytes after it, is inside
+        assert lay["exp_bytes"] >= n_bytes * threads * blocks + 4
+        assert lay["exp_bytes"] >= (total_bits + 7) // 8
+        # the last slot's two words: slot B*T starts at bit 5*B*T
+        last_word = (5 * blocks * threads) // 32
+        assert lay["gap_bytes"] >= 4 * (last_word + 2)
+        assert lay["gap_bytes"] % 4 == 0
+
+
 # ---------------------------------------------------------------- plausibility
 def test_gaussian_statistics_resemble_the_paper():
     """Sanity, not parity: exponent entropy near 2.6 bits, a few dozen
