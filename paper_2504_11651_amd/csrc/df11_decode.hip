@@ -53,17 +53,19 @@ __global__ __launch_bounds__(64 * W) void df11_decode_wave_kernel(DecodeArgs a) 
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // block indices stay scalar
+    const uint32_t first_block = xcd_grouped_index(blockIdx.x, gridDim.x) * W + wave;
+    const uint32_t stride = gridDim.x * W;
+    // the first block's words are requested before the tables are staged,
+    // so the two memory round trips overlap
+    ChunkWords cw{};
+    if (first_block < a.num_blocks) cw = load_chunk(a, first_block, first_block * 64u + lane);
     stage_table_blob(a, lds, tid, 64 * W);
     const Tables tb = stage_tables(a, lds);
     uint8_t *buf = lds + a.table_lds_bytes + wave * a.buf_bytes;
     uint32_t *buf32 = reinterpret_cast<uint32_t *>(buf);
     const uint32_t cap = a.buf_bytes - 8u;
     __syncthreads();
-
-    const uint32_t first_block = xcd_grouped_index(blockIdx.x, gridDim.x) * W + wave;
-    const uint32_t stride = gridDim.x * W;
     if (first_block >= a.num_blocks) return;
-    ChunkWords cw = load_chunk(a, first_block, first_block * 64u + lane);
     Chunk ch = chunk_setup(a, cw, first_block * 64u + lane);
     Range r = block_range(a, cw);
 
