@@ -56,6 +56,28 @@ def workload(name: str):
     raise SystemExit(f"unknown workload {name}")
 
 
+# weights per workload (the generators' output sizes), so that a workload's
+# layout is known without generating it
+WORKLOAD_WEIGHTS = {
+    "matrix_4096": 4096 * 4096,
+    "llama3_8b_block": 218_103_808,
+    "heavy_tailed_block": 218_103_808,
+    "llama31_70b_block": 855_638_016,
+}
+
+
+def layout_for(n: int, args=None):
+    """The library's layout for n weights (df11_default_layout), with the
+    --threads / --lut-bits overrides when given."""
+    from paper_2504_11651_amd import codec
+    lay = codec.default_layout(n)
+    if args is not None and args.threads:
+        lay.threads_per_block = args.threads
+    if args is not None and args.lut_bits:
+        lay.lut_bits = args.lut_bits
+    return lay
+
+
 def stack_mats():
     from paper_2504_11651_amd import synth
     mats, off = [], 0
@@ -133,21 +155,32 @@ def run_stack(args) -> int:
                                          stream=stream)
     fused = None
     if T == 1:
-        # fused decode-and-multiply (weights never written out), same step
-        gws = torch.empty(max(max(codec.gemv_workspace_bytes(d, mats) for d in streams) // 4, 4),
+        # fused decode-and-multiply (weights never written out), same step; it
+        # decodes 64-chunk blocks, so the stack is encoded once more for it
+        fstreams, fcomp = [], []
+        for i in range(blocks):
+            w, _ = synth.llama3_8b_stack_block(i)
+            hs = codec.encode(w, layout=codec.make_layout(*codec.FUSED_LAYOUT))
+            z = hs.sizes
+            fcomp.append((int(z.total_bits) + 7) // 8 + n + int(z.gap_bytes) +
+                         int(z.block_pos_bytes) + int(z.table_bytes))
+            fstreams.append(codec.to_device(hs, dev))
+        del hs
+        gws = torch.empty(max(max(codec.gemv_workspace_bytes(d, mats) for d in fstreams) // 4, 4),
                           dtype=torch.float32, device=dev)
         xs1 = [x.reshape(-1) for x in xs]
         ys1 = [torch.empty(r, dtype=torch.float32, device=dev) for _, r, _ in mats]
-        codec.block_gemv(streams[0], mats, xs1, ys1, gws, stream=stream)
+        codec.block_gemv(fstreams[0], mats, xs1, ys1, gws, stream=stream)
         torch.cuda.synchronize()
         codec.block_forward(streams[0], work, mats, xs, ys, ws, stream=stream)
         torch.cuda.synchronize()
         fused_rel = max(float((a - b.reshape(-1)).norm() / b.norm()) for a, b in zip(ys1, ys))
-        fstep = lambda i: codec.block_gemv(streams[i % blocks], mats, xs1, ys1, gws, stream=stream)
+        fstep = lambda i: codec.block_gemv(fstreams[i % blocks], mats, xs1, ys1, gws, stream=stream)
         f_wall, f_ms = timed(fstep, args.steps)
         fused = {"ms_per_step": round(f_wall, 5), "kernel_ms": round(f_ms, 5),
+                 "layout": ",".join(str(v) for v in codec.FUSED_LAYOUT),
                  "bf16_gbs_equivalent": round(2.0 * n / (f_wall * 1e-3) / 1e9, 2),
-                 "compressed_gbs": round(mean_comp_bytes() / (f_ms * 1e-3) / 1e9, 1),
+                 "compressed_gbs": round(float(np.mean(fcomp)) / (f_ms * 1e-3) / 1e9, 1),
                  "max_rel_diff_vs_unfused": fused_rel}
     dec = lambda i: codec.decode_block(streams[i % blocks], work, stream=stream)
     gemm = lambda i: codec.block_gemm(work, mats, xs, ys, ws, stream=stream)
@@ -278,7 +311,8 @@ def run_sweep(args) -> int:
         t_h2d = float(np.median(h2d))
         algo = hs.compressed_bytes + 2 * n
         comp_h2d_ms = t_h2d * hs.compressed_bytes / (2.0 * n)
-        rec = {"rows": rows, "weights": n, "bit_exact": exact,
+        rec = {"rows": rows, "weights": n, "threads_per_block": int(hs.layout.threads_per_block),
+               "bit_exact": exact,
                "decode_ms": round(t_dec, 5),
                "decode_ms_min_max": [round(float(dec.min()), 5), round(float(dec.max()), 5)],
                "decode_bf16_gbs": round(2.0 * n / (t_dec * 1e-3) / 1e9, 1),
@@ -570,6 +604,7 @@ def measure_decode(name: str, w: np.ndarray, lay, args, dev, flush, full: bool) 
     traffic = profiled_traffic(name, lay)
     rec = {
         "weights": n,
+        "layout": f"{lay.bytes_per_thread},{lay.threads_per_block},{lay.lut_bits}",
         "bit_exact": bit_exact,
         "ms": {"cold_median": round(med, 5), "cold_min": round(float(cold.min()), 5),
                "cold_max": round(float(cold.max()), 5), "cold_mean": round(float(cold.mean()), 5),
@@ -705,7 +740,6 @@ def main() -> int:
         return run_sweep(args)
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream(dev)
-    lay = codec.make_layout(8, args.threads, args.lut_bits)
     flush = torch.ones(1 << 28, dtype=torch.int32, device=dev)  # 1 GiB
 
     per_config = {}
@@ -714,12 +748,14 @@ def main() -> int:
             if name == args.workload:
                 continue
             wk = workload(name)
-            per_config[name] = measure_decode(name, wk, lay, args, dev, flush, full=False)
+            per_config[name] = measure_decode(name, wk, layout_for(wk.size, args), args, dev,
+                                              flush, full=False)
             del wk
 
     t0 = time.perf_counter()
     w = workload(args.workload)
     t_gen = time.perf_counter() - t0
+    lay = layout_for(w.size, args)
     head = measure_decode(args.workload, w, lay, args, dev, flush, full=True)
     hs = head.pop("_hs")
     timed_region_s = head.pop("timed_region_s")

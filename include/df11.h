@@ -122,6 +122,16 @@ int df11_build_codebook(const uint16_t *bf16, uint64_t n, uint32_t max_code_len,
 int df11_codebook_from_counts(const uint64_t counts[256], uint32_t max_code_len,
                               df11_codebook *out);
 
+/* The layout df11_decode_block decodes fastest for a stream of n weights:
+ * n = 8 bytes per thread and an 11-bit table index, with T = 128 threads per
+ * block from DF11_LARGE_STREAM_ELEMS weights up (one wavefront decodes a
+ * block, two chunks per lane) and T = 64 below (a shorter stream then
+ * finishes in fewer rounds of blocks).  T is a format parameter the paper
+ * leaves open (Sec. 2.3.2); it is recorded in the stream.  Host.  Returns
+ * DF11_E_INVALID_ARG for a null out. */
+#define DF11_LARGE_STREAM_ELEMS (192ull << 20)
+int df11_default_layout(uint64_t n, df11_layout *out);
+
 /* Buffer sizes for encoding the weights counted in cb with layout lay.
  * max_elems_per_block is left 0 (it depends on the data).  Host. */
 int df11_encoded_sizes(const df11_codebook *cb, const df11_layout *lay, df11_sizes *out);

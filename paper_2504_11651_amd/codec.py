@@ -24,7 +24,8 @@ ERRORS = {
 
 # every function include/df11.h declares
 EXPORTS = (
-    "df11_build_codebook", "df11_codebook_from_counts", "df11_encoded_sizes", "df11_encode",
+    "df11_build_codebook", "df11_codebook_from_counts", "df11_default_layout",
+    "df11_encoded_sizes", "df11_encode",
     "df11_build_tables", "df11_validate", "df11_decode_block", "df11_decode_launch_shape",
     "df11_gemm_workspace_bytes", "df11_block_gemm", "df11_block_forward",
     "df11_block_forward_noalloc", "df11_gemv_workspace_bytes", "df11_block_gemv", "df11_strerror",
@@ -81,7 +82,12 @@ class Matrix(ctypes.Structure):
     _fields_ = [("offset", ctypes.c_uint64), ("rows", ctypes.c_uint32), ("cols", ctypes.c_uint32)]
 
 
-DEFAULT_LAYOUT = (8, 64, 11)  # bytes per thread, threads per block, table index bits
+# bytes per thread, threads per block, table index bits, where no weight count
+# is at hand: the layout of large streams (128-chunk blocks, decoded one per
+# wavefront, two chunks per lane).  encode() takes default_layout(n).
+DEFAULT_LAYOUT = (8, 128, 11)
+# The fused decode-and-multiply path decodes 64-chunk blocks only.
+FUSED_LAYOUT = (8, 64, 11)
 
 _lib = None
 
@@ -107,6 +113,7 @@ def lib():
     sig = {
         "df11_build_codebook": [vp, u64, ctypes.c_uint32, P(Codebook)],
         "df11_codebook_from_counts": [vp, ctypes.c_uint32, P(Codebook)],
+        "df11_default_layout": [u64, P(Layout)],
         "df11_encoded_sizes": [P(Codebook), P(Layout), P(Sizes)],
         "df11_encode": [vp, u64, P(Codebook), P(Layout), vp, u64, vp, u64, vp, u64, vp, u64,
                         P(Sizes)],
@@ -156,6 +163,13 @@ def _ptr(a: np.ndarray):
 def make_layout(bytes_per_thread=None, threads_per_block=None, lut_bits=None) -> Layout:
     n, T, K = DEFAULT_LAYOUT
     return Layout(bytes_per_thread or n, threads_per_block or T, lut_bits or K)
+
+
+def default_layout(n: int) -> Layout:
+    """The library's layout for a stream of n weights (df11_default_layout)."""
+    lay = Layout()
+    _check(lib().df11_default_layout(int(n), ctypes.byref(lay)), "df11_default_layout")
+    return lay
 
 
 # ---------------------------------------------------------------- host side
@@ -220,7 +234,7 @@ def encode(w, cb: Codebook | None = None, layout: Layout | None = None,
            max_code_len: int = 32) -> HostStream:
     """Code book (unless given), stream, metadata and tables for BF16 bit patterns."""
     w = _u16(w)
-    layout = layout or make_layout()
+    layout = layout or default_layout(w.size)
     if cb is None:
         cb = build_codebook(w, max_code_len)
     z = encoded_sizes(cb, layout)
@@ -421,7 +435,8 @@ def gemv_workspace_bytes(ds: DeviceStream, mats) -> int:
 def block_gemv(ds: DeviceStream, mats, xs, ys, workspace=None, stream=None):
     """ys[m][r] = sum_k xs[m][k] * W_m[r][k] for one token, with the weights of
     ``ds`` decoded on chip (never written out).  xs[m]: bf16 (cols,) or
-    (1, cols); ys[m]: fp32 (rows,) or (1, rows)."""
+    (1, cols); ys[m]: fp32 (rows,) or (1, rows).  ``ds`` must be encoded in
+    FUSED_LAYOUT (64 chunks per block)."""
     import torch
     if not (len(mats) == len(xs) == len(ys)) or not mats:
         raise ValueError("one activation and one output tensor per matrix")

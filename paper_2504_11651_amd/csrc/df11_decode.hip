@@ -102,7 +102,71 @@ __global__ __launch_bounds__(64 * W) void df11_decode_wave_kernel(DecodeArgs a) 
     }
 }
 
-// T >= 128: one workgroup of T threads per block.
+// Lookups kept per chunk and sign/mantissa groups fetched at block start
+// when a lane owns two chunks (a 128-chunk block holds about twice the
+// outputs of a 64-chunk one).
+constexpr int kKeepPair = 10;
+constexpr int kPrePair = 7;
+
+// T = 128: one wave per block as well, lane l owning chunks 2l and 2l+1 of
+// it.  Its 16 bytes come in one 128-bit load, the two chunks decode
+// interleaved (independent table lookups in flight together), and the
+// block's count scan, buffer, edges and positions are shared by twice the
+// outputs.
+template <uint32_t W>
+__global__ __launch_bounds__(64 * W) void df11_decode_pair_kernel(DecodeArgs a) {
+    extern __shared__ __align__(16) uint8_t lds[];
+    const uint32_t tid = threadIdx.x;
+    const uint32_t lane = tid & 63u;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const uint32_t first_block = xcd_grouped_index(blockIdx.x, gridDim.x) * W + wave;
+    const uint32_t stride = gridDim.x * W;
+    PairWords pw{};
+    if (first_block < a.num_blocks) pw = load_pair(a, first_block, first_block * 128u + 2u * lane);
+    stage_table_blob(a, lds, tid, 64 * W);
+    const Tables tb = stage_tables(a, lds);
+    uint8_t *buf = lds + a.table_lds_bytes + wave * a.buf_bytes;
+    uint32_t *buf32 = reinterpret_cast<uint32_t *>(buf);
+    const uint32_t cap = a.buf_bytes - 8u;
+    __syncthreads();
+    if (first_block >= a.num_blocks) return;
+    Chunk A, B;
+    pair_setup(a, pw, first_block * 128u + 2u * lane, A, B);
+    Range r = block_range(a, pw.bp0, pw.bp1);
+
+    for (uint32_t b = first_block; b < a.num_blocks; b += stride) {
+        const uint32_t bn = b + stride;
+        PairWords nxt = pw;
+        if (bn < a.num_blocks) nxt = load_pair(a, bn, bn * 128u + 2u * lane);
+        uint2 S[kPrePair];
+        prefetch_sm(a, r, lane, 64u, S);
+        const uint32_t edge_sm = prefetch_edge_sm(a, r, lane);
+
+        wave_lds_sync();
+        for (uint32_t i = lane; i < (a.buf_bytes >> 4); i += 64u)
+            reinterpret_cast<uint4 *>(buf)[i] = make_uint4(0u, 0u, 0u, 0u);
+
+        uint32_t syA[kKeepPair], npkA[(kKeepPair + 3) / 4], syB[kKeepPair],
+            npkB[(kKeepPair + 3) / 4], restA, restB, cntA, cntB;
+        decode_count_pair(tb, A, B, syA, npkA, syB, npkB, &restA, &restB, &cntA, &cntB);
+        const uint32_t cnt = cntA + cntB;
+        const uint32_t excl = wave_inclusive_scan(cnt) - cnt;
+        __builtin_amdgcn_s_setprio(1);
+        wave_lds_sync();
+        emit_exponents(tb, A, syA, npkA, restA, r.shift + excl, buf32, cap);
+        emit_exponents(tb, B, syB, npkB, restB, r.shift + excl + cntA, buf32, cap);
+        wave_lds_sync();
+
+        __builtin_amdgcn_s_setprio(2);
+        assemble_block(a, r, buf, lane, 64u, S, edge_sm);
+        __builtin_amdgcn_s_setprio(0);
+        pw = nxt;
+        pair_setup(a, pw, bn * 128u + 2u * lane, A, B);
+        r = block_range(a, pw.bp0, pw.bp1);
+    }
+}
+
+// T >= 256: one workgroup of T threads per block.
 template <uint32_t T>
 __global__ __launch_bounds__(T) void df11_decode_block_kernel(DecodeArgs a) {
     extern __shared__ __align__(16) uint8_t lds[];
@@ -162,7 +226,7 @@ struct LaunchShape {
 struct DeviceInfo {
     int cus = 0;
     int max_lds = 0;                 // bytes of LDS one workgroup may use
-    uint32_t lds_granted[9] = {};    // dynamic LDS limit set per kernel instance
+    uint32_t lds_granted[11] = {};   // dynamic LDS limit set per kernel instance (slot)
     std::vector<LaunchShape> shapes; // launch shapes already worked out
 };
 
@@ -187,12 +251,22 @@ KernelFn wave_kernel(uint32_t W) {
     }
 }
 
+KernelFn pair_kernel(uint32_t W) {
+    switch (W) {
+        case 4: return df11_decode_pair_kernel<4>;
+        case 8: return df11_decode_pair_kernel<8>;
+        case 12: return df11_decode_pair_kernel<12>;
+        case 16: return df11_decode_pair_kernel<16>;
+        default: return nullptr;
+    }
+}
+
+// Slots of lds_granted: 0-3 wave kernels, 4-7 pair kernels, 8-10 below.
 KernelFn block_kernel(uint32_t T, int *slot) {
     switch (T) {
-        case 128: *slot = 4; return df11_decode_block_kernel<128>;
-        case 256: *slot = 5; return df11_decode_block_kernel<256>;
-        case 512: *slot = 6; return df11_decode_block_kernel<512>;
-        case 1024: *slot = 7; return df11_decode_block_kernel<1024>;
+        case 256: *slot = 8; return df11_decode_block_kernel<256>;
+        case 512: *slot = 9; return df11_decode_block_kernel<512>;
+        case 1024: *slot = 10; return df11_decode_block_kernel<1024>;
         default: return nullptr;
     }
 }
@@ -236,17 +310,19 @@ int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *bloc
         if (ls.threads == T && ls.lut_bits == K && ls.buf == buf) found = &ls;
     if (!found) {
         LaunchShape ls{T, K, buf, nullptr, 0, 0, 0, 1};
-        if (T == 64) {
-            // most resident waves per CU; fewer waves per workgroup on a tie
+        if (T == 64 || T == 128) {
+            // one wave per block: most resident waves per CU; fewer waves per
+            // workgroup on a tie
             int best_waves = 0;
             for (int i = 0; i < 4; ++i) {
                 const uint32_t W = kWaveChoices[i];
+                const KernelFn fn = T == 64 ? wave_kernel(W) : pair_kernel(W);
                 int pc = 0;
-                int rc = fit(di, i, wave_kernel(W), 64 * W, tab + W * buf, &pc);
+                int rc = fit(di, T == 64 ? i : 4 + i, fn, 64 * W, tab + W * buf, &pc);
                 if (rc) return rc;
                 if (pc * static_cast<int>(W) > best_waves) {
                     best_waves = pc * static_cast<int>(W);
-                    ls.fn = wave_kernel(W);
+                    ls.fn = fn;
                     ls.block = 64 * W;
                     ls.lds = tab + W * buf;
                     ls.per_cu = static_cast<uint32_t>(pc);
@@ -276,7 +352,7 @@ int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *bloc
     const uint64_t blocks_needed = (nb + W - 1) / W;
     uint64_t per_cu = found->per_cu;
     const uint64_t cap = kLongWavesPerSimd * 4 / W;  // 4 SIMDs per CU
-    if (T == 64 && cap >= 1 && per_cu > cap) {
+    if (T <= 128 && cap >= 1 && per_cu > cap) {
         const uint64_t cus = static_cast<uint64_t>(di.cus);
         const uint64_t rounds_all = (nb + cus * per_cu * W - 1) / (cus * per_cu * W);
         const uint64_t rounds_cap = (nb + cus * cap * W - 1) / (cus * cap * W);

@@ -195,6 +195,134 @@ __device__ __forceinline__ uint2 lookup(const Tables &t, const Chunk &ch, uint32
     return e;
 }
 
+// ---- two chunks per lane (blocks of 128 chunks decoded by one wavefront) ----
+
+// Raw global words for the chunk pair (c, c+1), c even: their 16 bytes (one
+// 128-bit load), the next 4 bytes, the two 32-bit words holding Gaps[c],
+// Gaps[c+1] and Gaps[c+2], and the block's two BlockOutputPos entries.
+struct PairWords {
+    uint32_t x0, x1, x2, x3, z, g0, g1, bp0, bp1;
+};
+
+__device__ __forceinline__ PairWords load_pair(const DecodeArgs &a, uint32_t b, uint32_t c) {
+    PairWords r;
+    const __attribute__((address_space(4))) uint32_t *bp =
+        (const __attribute__((address_space(4))) uint32_t *)a.block_pos;
+    r.bp0 = bp[b];
+    r.bp1 = bp[b + 1];
+    const uint4 own = *reinterpret_cast<const uint4 *>(a.exp + 8ull * c);
+    r.x0 = own.x;
+    r.x1 = own.y;
+    r.x2 = own.z;
+    r.x3 = own.w;
+    r.z = *reinterpret_cast<const uint32_t *>(a.exp + 8ull * c + 16);
+    const uint64_t gw = (5ull * c) >> 5;
+    r.g0 = a.gaps[gw];
+    r.g1 = a.gaps[gw + 1];
+    return r;
+}
+
+// Decode state of chunks c (A) and c+1 (B).  B's window words start at the
+// pair's third word; their low 3 shifted-in bits come from A's bits and only
+// ever sit below a window's table index, which is masked off.
+__device__ __forceinline__ void pair_setup(const DecodeArgs &a, const PairWords &pw, uint32_t c,
+                                           Chunk &A, Chunk &B) {
+    const uint32_t w0 = lsb_first(pw.x0), w1 = lsb_first(pw.x1), w2 = lsb_first(pw.x2),
+                   w3 = lsb_first(pw.x3), w4 = lsb_first(pw.z);
+    const uint32_t s2 = __builtin_amdgcn_alignbit(w2, w1, 29);
+    A.w0 = w0;
+    A.w1 = w1;
+    A.w2 = w2;
+    A.s0 = w0 << 3;
+    A.s1 = __builtin_amdgcn_alignbit(w1, w0, 29);
+    A.s2 = s2;
+    B.w0 = w2;
+    B.w1 = w3;
+    B.w2 = w4;
+    B.s0 = s2;
+    B.s1 = __builtin_amdgcn_alignbit(w3, w2, 29);
+    B.s2 = __builtin_amdgcn_alignbit(w4, w3, 29);
+    const uint64_t gv = ((static_cast<uint64_t>(__builtin_bswap32(pw.g0)) << 32) |
+                         __builtin_bswap32(pw.g1))
+                        << ((5u * c) & 31u);
+    const uint32_t gap_a = static_cast<uint32_t>(gv >> 59);
+    const uint32_t gap_b = static_cast<uint32_t>(gv >> 54) & 31u;
+    const uint32_t gap_c = static_cast<uint32_t>(gv >> 49) & 31u;
+    A.start = A.end = B.start = B.end = 0;
+    if (c < a.num_chunks) {
+        A.start = gap_a;
+        const uint32_t e = (c + 1 < a.num_chunks) ? 64u + gap_b
+                                                  : static_cast<uint32_t>(a.total_bits - 64ull * c);
+        A.end = min(e, 95u);
+    }
+    if (c + 1 < a.num_chunks) {
+        B.start = gap_b;
+        const uint32_t e = (c + 2 < a.num_chunks)
+                               ? 64u + gap_c
+                               : static_cast<uint32_t>(a.total_bits - 64ull * (c + 1));
+        B.end = min(e, 95u);
+    }
+}
+
+// Phase 1 for both chunks of a pair at once: each step takes one lookup of
+// A and one of B, which are independent, so their LDS round trips overlap.
+// Otherwise as decode_count, per chunk.
+template <int N>
+__device__ __forceinline__ void decode_count_pair(const Tables &t, const Chunk &A, const Chunk &B,
+                                                  uint32_t (&syA)[N], uint32_t (&npkA)[(N + 3) / 4],
+                                                  uint32_t (&syB)[N], uint32_t (&npkB)[(N + 3) / 4],
+                                                  uint32_t *restA, uint32_t *restB,
+                                                  uint32_t *cntA, uint32_t *cntB) {
+#pragma unroll
+    for (int k = 0; k < (N + 3) / 4; ++k) npkA[k] = npkB[k] = 0u;
+    uint32_t pA = A.start, pB = B.start, cA = 0, cB = 0;
+    uint32_t lpA = 0, lmA = 0, lpB = 0, lmB = 0;
+    constexpr uint32_t sel[4] = {0x03020105u, 0x03020500u, 0x03050100u, 0x05020100u};
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+        const bool actA = pA < A.end, actB = pB < B.end;
+        syA[k] = syB[k] = 0u;
+        if (__builtin_amdgcn_ballot_w64(actA || actB) == 0) continue;  // wave-uniform skip
+        const uint32_t wsA = window_at(A.s0, A.s1, A.s2, pA);
+        const uint32_t wsB = window_at(B.s0, B.s1, B.s2, pB);
+        uint2 eA = lds_entry(wsA & t.addr_mask);
+        uint2 eB = lds_entry(wsB & t.addr_mask);
+        if (actA && eA.y == 0u) eA = decode_long(t, window_at(A.w0, A.w1, A.w2, pA));
+        if (actB && eB.y == 0u) eB = decode_long(t, window_at(B.w0, B.w1, B.w2, pB));
+        const uint32_t mA = actA ? eA.y : 0u, mB = actB ? eB.y : 0u;
+        syA[k] = eA.x;
+        syB[k] = eB.x;
+        npkA[k / 4] = __builtin_amdgcn_perm(mA, npkA[k / 4], sel[k % 4]);  // byte k%4 <- count
+        npkB[k / 4] = __builtin_amdgcn_perm(mB, npkB[k / 4], sel[k % 4]);
+        lpA = actA ? pA : lpA;
+        lmA = actA ? mA : lmA;
+        lpB = actB ? pB : lpB;
+        lmB = actB ? mB : lmB;
+        pA += eA.y & 0xFFu;  // done chunks only move further past their end
+        pB += eB.y & 0xFFu;
+        cA += (mA >> 8) & 0xFFu;
+        cB += (mB >> 8) & 0xFFu;
+    }
+    *restA = pA;
+    *restB = pB;
+    for (uint32_t it = 0; pA < A.end && it < 96u; ++it) {
+        const uint2 e = lookup(t, A, pA);
+        lpA = pA;
+        lmA = e.y;
+        pA += e.y & 0xFFu;
+        cA += (e.y >> 8) & 0xFFu;
+    }
+    for (uint32_t it = 0; pB < B.end && it < 96u; ++it) {
+        const uint2 e = lookup(t, B, pB);
+        lpB = pB;
+        lmB = e.y;
+        pB += e.y & 0xFFu;
+        cB += (e.y >> 8) & 0xFFu;
+    }
+    *cntA = cA - __builtin_popcount((lmA >> 16) >> min(A.end - lpA, 31u));
+    *cntB = cB - __builtin_popcount((lmB >> 16) >> min(B.end - lpB, 31u));
+}
+
 // Phase 1: decode the codes that start in the chunk, keep up to kKeep
 // lookups (exponent words in sy, code counts one byte each in npk), and
 // count the codes.  Returns the count; *p_rest = where decoding stopped.
@@ -246,14 +374,15 @@ __device__ __forceinline__ void or_exponents(uint32_t *buf32, uint32_t off, uint
 // holds at most 4 codes, so 3 bits of each kept count suffice; with the start
 // clamped, the kept lookups stay inside the buffer whatever the metadata and
 // tables hold; the rest are clamped one by one.
+template <int N>
 __device__ __forceinline__ void emit_exponents(const Tables &t, const Chunk &ch,
-                                               const uint32_t (&sy)[kKeep],
-                                               const uint32_t (&npk)[(kKeep + 3) / 4],
+                                               const uint32_t (&sy)[N],
+                                               const uint32_t (&npk)[(N + 3) / 4],
                                                uint32_t p_rest, uint32_t off, uint32_t *buf32,
                                                uint32_t cap_bytes) {
-    off = umin(off, cap_bytes - 8u * kKeep);
+    off = umin(off, cap_bytes - 8u * N);
 #pragma unroll
-    for (int k = 0; k < kKeep; ++k) {
+    for (int k = 0; k < N; ++k) {
         const uint32_t n = (npk[k / 4] >> (8 * (k % 4))) & 7u;
         if (n != 0u) {
             or_exponents(buf32, off, sy[k]);
@@ -280,10 +409,10 @@ struct Range {
     uint32_t s, shift, lim, g0, ngroups, full_lo, full_hi;
 };
 
-__device__ __forceinline__ Range block_range(const DecodeArgs &a, const ChunkWords &cw) {
+__device__ __forceinline__ Range block_range(const DecodeArgs &a, uint32_t bp0, uint32_t bp1) {
     Range r;
-    r.s = umin(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(cw.bp0)), a.n_elems);
-    uint32_t e = umax(umin(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(cw.bp1)), a.n_elems), r.s);
+    r.s = umin(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(bp0)), a.n_elems);
+    uint32_t e = umax(umin(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(bp1)), a.n_elems), r.s);
     // at most the buffer's worth; the room above r.s is clamped so the sum
     // cannot wrap for a stream ending near 2^32 weights
     e = umin(e, r.s + umin(a.buf_bytes - kBufSlack, 0xFFFFFFFFu - r.s));
@@ -296,18 +425,23 @@ __device__ __forceinline__ Range block_range(const DecodeArgs &a, const ChunkWor
     return r;
 }
 
+__device__ __forceinline__ Range block_range(const DecodeArgs &a, const ChunkWords &cw) {
+    return block_range(a, cw.bp0, cw.bp1);
+}
+
 __device__ __forceinline__ bool full_group(const Range &r, uint32_t g) {
     return g - r.full_lo < r.full_hi - r.full_lo;  // full_lo <= g < full_hi
 }
 
-// Sign/mantissa bytes of groups first, first+step, ... (kPre of them).  The
+// Sign/mantissa bytes of groups first, first+step, ... (P of them).  The
 // buffer is zero padded past n_elems to a multiple of 16 bytes, so a whole
 // group can be read even where the block starts or ends inside it.
+template <int P>
 __device__ __forceinline__ void prefetch_sm(const DecodeArgs &a, const Range &r, uint32_t first,
-                                            uint32_t step, uint2 (&S)[kPre]) {
+                                            uint32_t step, uint2 (&S)[P]) {
     const uint32_t last = umax(r.ngroups, 1u) - 1u;  // groups past the block reread its last one
 #pragma unroll
-    for (int k = 0; k < kPre; ++k) {
+    for (int k = 0; k < P; ++k) {
         const uint32_t g = umin(first + k * step, last);
         S[k] = *reinterpret_cast<const uint2 *>(a.sm + r.g0 + (g << 3));
     }
@@ -348,28 +482,29 @@ __device__ __forceinline__ void store_group(const DecodeArgs &a, const Range &r,
 }
 
 // Assemble and store every whole group of the block: groups first + k*step.
-// The first kPre use the bytes fetched when the block started.  Loads and
+// The first P use the bytes fetched when the block started.  Loads and
 // stores share one in-order counter on this GPU, so all of those groups are
 // assembled (their loads waited for) before the first store is issued;
 // otherwise each wait would also wait for the stores issued before it.
 // Then the elements of the (at most two) partial groups that this block
 // owns go out as one 2-byte store instruction over threads 0..15.
+template <int P>
 __device__ __forceinline__ void assemble_block(const DecodeArgs &a, const Range &r,
                                                const uint8_t *buf, uint32_t first, uint32_t step,
-                                               const uint2 (&S)[kPre], uint32_t edge_sm) {
-    uint4 O[kPre];
+                                               const uint2 (&S)[P], uint32_t edge_sm) {
+    uint4 O[P];
 #pragma unroll
-    for (int k = 0; k < kPre; ++k) {
+    for (int k = 0; k < P; ++k) {
         const uint32_t g = first + k * step;
         O[k] = make_uint4(0u, 0u, 0u, 0u);
         if (full_group(r, g)) O[k] = assemble_group(buf, g, S[k]);
     }
 #pragma unroll
-    for (int k = 0; k < kPre; ++k) {
+    for (int k = 0; k < P; ++k) {
         const uint32_t g = first + k * step;
         if (full_group(r, g)) store_group(a, r, g, O[k]);
     }
-    for (uint32_t g = first + kPre * step; g < r.full_hi; g += step)
+    for (uint32_t g = first + P * step; g < r.full_hi; g += step)
         if (full_group(r, g))
             store_group(a, r, g,
                         assemble_group(buf, g, *reinterpret_cast<const uint2 *>(a.sm + r.g0 + (g << 3))));

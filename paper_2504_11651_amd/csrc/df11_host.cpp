@@ -258,6 +258,14 @@ int df11_build_codebook(const uint16_t *bf16, uint64_t n, uint32_t max_code_len,
     return df11_codebook_from_counts(counts, max_code_len, out);
 }
 
+int df11_default_layout(uint64_t n, df11_layout *out) {
+    if (!out) return DF11_E_INVALID_ARG;
+    out->bytes_per_thread = 8;
+    out->threads_per_block = n >= DF11_LARGE_STREAM_ELEMS ? 128 : 64;
+    out->lut_bits = 11;
+    return DF11_OK;
+}
+
 int df11_encoded_sizes(const df11_codebook *cb, const df11_layout *lay, df11_sizes *out) {
     if (!cb || !out || !layout_ok(lay)) return DF11_E_INVALID_ARG;
     uint64_t n = 0, bits = 0;

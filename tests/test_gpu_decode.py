@@ -25,8 +25,8 @@ CASES = {
     "fib24": lambda: synth.fibonacci_exponents(24),
     "heavy": lambda: synth.heavy_tailed_block(500_000, 2),
 }
-LAYOUTS = [(8, 64, 8), (8, 64, 11), (8, 64, 12), (8, 128, 10), (8, 256, 12), (8, 512, 11),
-           (8, 1024, 12)]
+LAYOUTS = [(8, 64, 8), (8, 64, 11), (8, 64, 12), (8, 128, 8), (8, 128, 10), (8, 128, 11),
+           (8, 128, 12), (8, 256, 12), (8, 512, 11), (8, 1024, 12)]
 
 
 def oracle_reference(w: np.ndarray, cap: int = 32) -> np.ndarray:

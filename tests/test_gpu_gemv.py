@@ -7,6 +7,8 @@ import pytest
 import oracle
 from paper_2504_11651_amd import codec, synth
 
+FUSED = codec.make_layout(*codec.FUSED_LAYOUT)  # the fused kernel decodes 64-chunk blocks
+
 from conftest import gpu_available
 
 pytestmark = [pytest.mark.gpu,
@@ -71,7 +73,7 @@ def test_block_gemv_matches_oracle_and_driver(name):
     # matrices must start 16-byte aligned: round the gaps up to multiples of 8
     gaps = tuple((g + 7) // 8 * 8 for g in gaps)
     w, mats = make_stream(kw["shapes"], len(name), gaps=gaps, const=kw.get("const"))
-    hs = codec.encode(w)
+    hs = codec.encode(w, layout=FUSED)
     ds = codec.to_device(hs, "cuda")
     xs_h = [synth.activations(1, c, 55, i) for i, (_, _, c) in enumerate(mats)]
     ys = run_gemv(ds, mats, xs_h)
@@ -103,7 +105,7 @@ def test_block_gemv_llama3_8b_block_every_output():
     import torch
     w, offs = synth.llama3_8b_block()
     mats = [(off, r, c) for off, r, c, _ in offs.values()]
-    ds = codec.to_device(codec.encode(w), "cuda")
+    ds = codec.to_device(codec.encode(w, layout=FUSED), "cuda")
     xs_h = [synth.activations(1, c, 56, i) for i, (_, _, c) in enumerate(mats)]
     ys = run_gemv(ds, mats, xs_h)
     xs = [torch.from_numpy(x.view(np.int16)).cuda().view(torch.bfloat16) for x in xs_h]
@@ -135,7 +137,7 @@ def test_random_streams_gemv(seed):
     shapes = [(int(rng.integers(2, 65)), 64 * int(rng.integers(32, 81))) for _ in range(k)]
     gaps = tuple(8 * int(rng.integers(0, 700)) if rng.random() < 0.5 else 0 for _ in range(k))
     w, mats = make_stream(shapes, 900 + seed, gaps=gaps)
-    ds = codec.to_device(codec.encode(w), "cuda")
+    ds = codec.to_device(codec.encode(w, layout=FUSED), "cuda")
     xs_h = [synth.activations(1, c, 950 + seed, i) for i, (_, _, c) in enumerate(mats)]
     ys = run_gemv(ds, mats, xs_h)
     check_oracle(w, mats, xs_h, ys)
@@ -151,7 +153,7 @@ def test_gemv_on_a_side_stream_without_workspace():
     not disturb it."""
     import torch
     w, mats = make_stream([(48, 4096), (16, 2048)], 1234)
-    ds = codec.to_device(codec.encode(w), "cuda")
+    ds = codec.to_device(codec.encode(w, layout=FUSED), "cuda")
     xs_h = [synth.activations(1, c, 1235, i) for i, (_, _, c) in enumerate(mats)]
     ref = run_gemv(ds, mats, xs_h)
     side = torch.cuda.Stream()

@@ -94,7 +94,7 @@ def test_block_gemv_replays_in_a_graph():
         mats.append((off, r, c))
         off += r * c
     w = synth.gaussian(off, 0.02, 85)
-    ds = codec.to_device(codec.encode(w), "cuda")
+    ds = codec.to_device(codec.encode(w, layout=codec.make_layout(*codec.FUSED_LAYOUT)), "cuda")
     xs = [torch.from_numpy(synth.activations(1, c, 86, m).view(np.int16)).cuda()
           .view(torch.bfloat16).reshape(-1) for m, (_, _, c) in enumerate(mats)]
     ys = [torch.empty(r, dtype=torch.float32, device="cuda") for _, r, _ in mats]

@@ -1,8 +1,10 @@
 """GPU parity at the largest stream the format allows: 2^32 - 1 weights (the
-output positions are 32-bit), in the default layout.  Every decoded weight is
-compared with the input, and the fused decode-and-multiply path is checked on
-sampled rows of a matrix that ends just before the stream does (the last
-block then reaches into weights that belong to no matrix)."""
+output positions are 32-bit), in the default layout (128-chunk blocks, two
+chunks per lane) and in the 64-chunk layout.  Every decoded weight is
+compared with the input, and the fused decode-and-multiply path (64-chunk
+blocks) is checked on sampled rows of a matrix that ends just before the
+stream does (the last block then reaches into weights that belong to no
+matrix)."""
 import numpy as np
 import pytest
 
@@ -17,14 +19,8 @@ pytestmark = [pytest.mark.gpu,
 N_MAX = 2 ** 32 - 1
 
 
-def test_largest_stream_decodes_bit_exact():
+def _decode_all(ds, w):
     import torch
-    print(f"generating {N_MAX} weights", flush=True)
-    w = synth.gaussian(N_MAX, 0.02, 2024)
-    hs = codec.encode(w)
-    assert codec.validate(hs) == 0
-    assert int(hs.block_pos[-1]) == N_MAX
-    ds = codec.to_device(hs, "cuda")
     out = torch.full((N_MAX,), 0x5A5A, dtype=torch.int16, device="cuda")
     codec.decode_block(ds, out.view(torch.bfloat16))
     torch.cuda.synchronize()
@@ -35,6 +31,23 @@ def test_largest_stream_decodes_bit_exact():
         pytest.fail(f"{int((~same).sum())} mismatches, first at {bad}")
     del out, ref, same
     torch.cuda.empty_cache()
+
+
+def test_largest_stream_decodes_bit_exact():
+    import torch
+    print(f"generating {N_MAX} weights", flush=True)
+    w = synth.gaussian(N_MAX, 0.02, 2024)
+    for lay in (codec.make_layout(), codec.make_layout(*codec.FUSED_LAYOUT)):
+        print(f"layout T={lay.threads_per_block}", flush=True)
+        hs = codec.encode(w, layout=lay)
+        assert codec.validate(hs) == 0
+        assert int(hs.block_pos[-1]) == N_MAX
+        ds = codec.to_device(hs, "cuda")
+        del hs
+        _decode_all(ds, w)
+        if lay.threads_per_block != codec.FUSED_LAYOUT[1]:
+            del ds
+            torch.cuda.empty_cache()
 
     # one matrix of 4096 columns covering all but the last 4095 weights
     rows, cols = N_MAX // 4096, 4096
