@@ -232,69 +232,87 @@ gemm_slab_kernel(GemmArgs a) {
     constexpr uint32_t kPieces = 16u * MT * kRowPieces;
     constexpr uint32_t kPer = kPieces / (64u * kSlabWaves);
     static_assert(kPieces % (64u * kSlabWaves) == 0, "whole pieces per thread");
+    // Inside the loop every slab has a next one, whose activations and
+    // weights are all requested before this slab's products wait for
+    // anything; loads complete in order, so the wait for one load never
+    // waits for loads issued after it.  Activations are masked when staged,
+    // not when they arrive (a use on arrival would wait for every older load).
     uint4 xr[kPer];
+    auto slab_piece = [&](uint32_t i, uint32_t k, uint32_t *t, uint32_t *kk) {
+        const uint32_t q = tid + 64u * kSlabWaves * i;
+        *t = q / kRowPieces;
+        *kk = k + 8u * (q % kRowPieces);
+        return *t < a.tokens && *kk < k1;
+    };
     auto load_slab = [&](uint32_t k) {
 #pragma unroll
         for (uint32_t i = 0; i < kPer; ++i) {
-            const uint32_t q = tid + 64u * kSlabWaves * i;
-            const uint32_t t = q / kRowPieces, kk = k + 8u * (q % kRowPieces);
-            const bool ok = t < a.tokens && kk < k1;
-            const uint4 v = load16(m.x + static_cast<uint64_t>(ok ? t : 0u) * m.cols + (ok ? kk : k0));
-            xr[i] = masked(v, ok ? ~0u : 0u);
+            uint32_t t, kk;
+            const bool ok = slab_piece(i, k, &t, &kk);
+            xr[i] = load16(m.x + static_cast<uint64_t>(ok ? t : 0u) * m.cols + (ok ? kk : k0));
         }
     };
-    auto store_slab = [&]() {
+    auto store_slab = [&](uint32_t k) {
 #pragma unroll
         for (uint32_t i = 0; i < kPer; ++i) {
+            uint32_t t, kk;
+            const bool ok = slab_piece(i, k, &t, &kk);
             const uint32_t q = tid + 64u * kSlabWaves * i;
             *reinterpret_cast<uint4 *>(slab + (q / kRowPieces) * kSlabStride + 16u * (q % kRowPieces)) =
-                xr[i];
+                masked(xr[i], ok ? ~0u : 0u);
         }
     };
-
+    // weights of 64-k step u of the slab at k (steps past the range repeat
+    // its last step: in bounds, and not used)
+    uint4 W[kUnroll][2];
+    auto load_w = [&](uint32_t u, uint32_t k) {
+        const uint32_t steps = umin(kUnroll, (k1 - k) / kKStep);
+        const uint32_t kk = k + kKStep * umin(u, steps - 1u);
+        W[u][0] = load16(wrow + kk);
+        W[u][1] = load16(wrow + kk + 32u);
+    };
     f32x4 acc[MT];
 #pragma unroll
     for (uint32_t mt = 0; mt < MT; ++mt) acc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    load_slab(k0);
-    store_slab();
-    __syncthreads();
-    for (uint32_t k = k0; k < k1; k += kSlabK) {
-        const uint32_t steps = umin(kUnroll, (k1 - k) / kKStep);  // uniform
-        uint4 W[kUnroll][2];
-        if (active) {
+    auto products = [&](uint32_t u) {
 #pragma unroll
-            for (uint32_t u = 0; u < kUnroll; ++u) {
-                const uint32_t kk = k + kKStep * umin(u, steps - 1u);  // in range
-                W[u][0] = load16(wrow + kk);
-                W[u][1] = load16(wrow + kk + 32u);
-            }
+        for (uint32_t mt = 0; mt < MT; ++mt) {
+            const uint8_t *row = slab + (16u * mt + j) * kSlabStride + 2u * (kKStep * u + 8u * g);
+            const uint4 x0 = *reinterpret_cast<const uint4 *>(row);
+            const uint4 x1 = *reinterpret_cast<const uint4 *>(row + 64u);
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x0), as_bf16x8(W[u][0]),
+                                                              acc[mt], 0, 0, 0);
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x1), as_bf16x8(W[u][1]),
+                                                              acc[mt], 0, 0, 0);
         }
-        const bool more = k + kSlabK < k1;
-        if (more) load_slab(k + kSlabK);
-        if (active) {
+    };
+
 #pragma unroll
-            for (uint32_t u = 0; u < kUnroll; ++u) {
-                if (u < steps) {
+    for (uint32_t u = 0; u < kUnroll; ++u) load_w(u, k0);
+    load_slab(k0);
+    store_slab(k0);
+    __syncthreads();
+    uint32_t k = k0;
+    for (; k + kSlabK < k1; k += kSlabK) {
+        const uint32_t kn = k + kSlabK;
+        load_slab(kn);
+        // each step's weight registers take the next slab's weights as soon
+        // as its products are issued: a wave keeps kUnroll steps of weights
+        // in flight across the barriers
 #pragma unroll
-                    for (uint32_t mt = 0; mt < MT; ++mt) {
-                        const uint8_t *row = slab + (16u * mt + j) * kSlabStride + 2u * (kKStep * u + 8u * g);
-                        const uint4 x0 = *reinterpret_cast<const uint4 *>(row);
-                        const uint4 x1 = *reinterpret_cast<const uint4 *>(row + 64u);
-                        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            as_bf16x8(x0), as_bf16x8(W[u][0]), acc[mt], 0, 0, 0);
-                        acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                            as_bf16x8(x1), as_bf16x8(W[u][1]), acc[mt], 0, 0, 0);
-                    }
-                }
-            }
+        for (uint32_t u = 0; u < kUnroll; ++u) {
+            if (active) products(u);
+            load_w(u, kn);
         }
         __syncthreads();  // every wave is done with this slab
-        if (more) {
-            store_slab();
-            __syncthreads();
-        }
+        store_slab(kn);
+        __syncthreads();
     }
+    // the last slab of the range
+    const uint32_t steps = umin(kUnroll, (k1 - k) / kKStep);  // uniform
+#pragma unroll
+    for (uint32_t u = 0; u < kUnroll; ++u)
+        if (active && u < steps) products(u);
     if (active) write_tile<MT>(a, m, rb, s, j, g, acc);
 }
 
