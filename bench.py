@@ -462,18 +462,48 @@ DECODER_SOURCES = ("paper_2504_11651_amd/csrc/df11_decode.hip",
                    "paper_2504_11651_amd/csrc/df11_tables.h")
 
 
+def code_only(src: str) -> str:
+    """C/C++ source text without its comments, whitespace runs collapsed: what
+    the compiler sees, so that a hash of it changes only with the code."""
+    out, i, n = [], 0, len(src)
+    while i < n:
+        if src.startswith("//", i):
+            j = src.find("\n", i)
+            i = n if j < 0 else j
+        elif src.startswith("/*", i):
+            j = src.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        elif src[i] in "\"'":
+            q, j = src[i], i + 1
+            while j < n and src[j] != q:
+                j += 2 if src[j] == "\\" else 1
+            out.append(src[i:j + 1])
+            i = j + 1
+        else:
+            out.append(src[i])
+            i += 1
+    return " ".join("".join(out).split())
+
+
+def decoder_source_sha256() -> str:
+    """sha256 of the decoder's code (its sources without comments), as the
+    committed counter summaries record it."""
+    import hashlib
+    h = hashlib.sha256()
+    for p in DECODER_SOURCES:
+        with open(os.path.join(ROOT, p), encoding="utf-8") as f:
+            h.update(code_only(f.read()).encode())
+    return h.hexdigest()
+
+
 def profiled_traffic(workload_name: str, lay) -> float | None:
     """HBM bytes per launch from the committed rocprofv3 counter summary of this
     workload and layout: FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each
     scaled by what the same counter reads for a 512 MiB copy.  None when no
-    summary exists or the decoder source changed since it was taken."""
+    summary exists or the decoder's code changed since it was taken."""
     import glob
-    import hashlib
-    h = hashlib.sha256()
-    for p in DECODER_SOURCES:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
-    want = {"workload": workload_name, "source_sha256": h.hexdigest(),
+    want = {"workload": workload_name, "source_sha256": decoder_source_sha256(),
             "layout": f"{lay.bytes_per_thread},{lay.threads_per_block},{lay.lut_bits}"}
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "df11_decode_*.md"))):
         kv = {}

@@ -2,19 +2,22 @@
 // re-designed for CDNA4).
 //
 // A block of T chunks (the paper's "thread block") is decoded by one
-// wavefront when T = 64 -- the block's prefix sum is then a wave-level DPP
-// scan and no workgroup barrier is needed, so the waves of a CU drift into
-// different phases and decode overlaps memory streaming -- or by one
-// workgroup when T >= 128.  The grid is persistent: decode tables are staged
-// into LDS once per workgroup and shared by all of its waves.
+// wavefront when T = 64 (a chunk per lane) or T = 128 (two adjacent chunks
+// per lane, decoded as two interleaved lookup chains) -- the block's prefix
+// sum is then a wave-level DPP scan and no workgroup barrier is needed, so
+// the waves of a CU drift into different phases and decode overlaps memory
+// streaming -- or by one workgroup when T >= 256.  The grid is persistent:
+// decode tables are staged into LDS once per workgroup and shared by all of
+// its waves.
 //
 // Per block:
 //   1. every lane loads its 8-byte chunk of EncodedExponent plus the next
-//      4 bytes, and its two 5-bit Gaps (own chunk and next chunk);
+//      4 bytes (or its two chunks' 16 bytes plus the next 4), and the 5-bit
+//      Gaps of its chunks and of the next chunk;
 //   2. phase 1 (count): starting at the gap, decode with the multi-symbol
 //      table until the code start reaches the next chunk's first code;
 //   3. exclusive scan of the counts (wave DPP scan, plus LDS across waves
-//      for T >= 128) gives each lane its output position (Sec. 2.3.2);
+//      for T >= 256) gives each lane its output position (Sec. 2.3.2);
 //   4. phase 2 (emit): replay the lookups phase 1 kept in registers (a
 //      chunk that needed more decodes its remaining codes again) and OR the
 //      exponent bytes into an LDS buffer at their output positions.  The

@@ -52,3 +52,13 @@ def test_default_layout_by_size():
     for n, T in ((0, 64), (1, 64), (big - 1, 64), (big, 128), (2 ** 32 - 1, 128)):
         lay = codec.default_layout(n)
         assert (lay.bytes_per_thread, lay.threads_per_block, lay.lut_bits) == (8, T, 11)
+
+
+def test_decoder_hash_follows_code_not_comments():
+    import bench
+    a = 'int f(int x) { return x + 1; }  // one\n/* block\n comment */\nconst char *s = "//";\n'
+    b = '// header\nint f(int x)  {\n  return x + 1;  /* inline */ }\nconst char *s = "//";\n'
+    c = 'int f(int x) { return x + 2; }\nconst char *s = "//";\n'
+    assert bench.code_only(a) == bench.code_only(b)
+    assert bench.code_only(a) != bench.code_only(c)
+    assert '"//"' in bench.code_only(a)  # string literals are code
