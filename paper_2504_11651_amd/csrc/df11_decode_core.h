@@ -210,7 +210,10 @@ __device__ __forceinline__ PairWords load_pair(const DecodeArgs &a, uint32_t b, 
         (const __attribute__((address_space(4))) uint32_t *)a.block_pos;
     r.bp0 = bp[b];
     r.bp1 = bp[b + 1];
-    const uint4 own = *reinterpret_cast<const uint4 *>(a.exp + 8ull * c);
+    // EncodedExponent is only 8-byte aligned (its stated alignment), and the
+    // type says so; the load stays one 16-byte load
+    typedef uint32_t u32x4_a8 __attribute__((ext_vector_type(4), aligned(8)));
+    const u32x4_a8 own = *reinterpret_cast<const u32x4_a8 *>(a.exp + 8ull * c);
     r.x0 = own.x;
     r.x1 = own.y;
     r.x2 = own.z;
