@@ -71,6 +71,38 @@ def test_long_codes_through_escape_path(cap, K):
     assert np.array_equal(got, ref)
 
 
+@pytest.mark.parametrize("T", [64, 128, 256])
+def test_launch_shape(T):
+    """The decoder's launch for a stream long enough to fill the GPU: with
+    T = 64 or 128 one wavefront per block, W = block/64 waves per workgroup
+    sharing the tables, LDS = tables + one output buffer per wave, a
+    persistent grid of whole CUs' worth of workgroups and at least 3 waves
+    per SIMD; with T = 256 one workgroup of T threads per block, LDS = tables
+    + 16 scan slots + one buffer.  The decode in that shape is bit-exact."""
+    import torch
+    w = synth.gaussian(40_000_000, 0.02, 5)
+    hs = codec.encode(w, layout=codec.make_layout(8, T, 11))
+    ds = codec.to_device(hs, "cuda")
+    grid, block, lds = codec.launch_shape(ds)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    nb = int(hs.sizes.num_blocks)
+    tables = (8 * 2048 + 2 * 4 * 33 + 256 + 15) // 16 * 16
+    buf = (int(hs.sizes.max_elems_per_block) + 128 + 15) // 16 * 16
+    if T <= 128:
+        W = block // 64
+        assert block % 64 == 0 and W in (4, 8, 12, 16)
+        assert lds == tables + W * buf
+        assert grid <= (nb + W - 1) // W and grid % cus == 0
+        assert grid * W >= 3 * 4 * cus  # at least 3 waves per SIMD
+    else:
+        assert block == T and lds == tables + 4 * 16 + buf
+        assert grid <= nb
+    out = torch.empty(w.size, dtype=torch.int16, device="cuda")
+    codec.decode_block(ds, out.view(torch.bfloat16))
+    torch.cuda.synchronize()
+    assert torch.equal(out, torch.from_numpy(w.view(np.int16)).cuda())
+
+
 def test_empty_stream_launches_nothing():
     import torch
     hs = codec.encode(np.zeros(0, np.uint16))

@@ -15,12 +15,15 @@ pytestmark = [pytest.mark.gpu,
               pytest.mark.skipif(not gpu_available(), reason="needs an MI355X")]
 
 
-def test_decode_block_replays_in_a_graph():
+@pytest.mark.parametrize("T", [64, 128])
+def test_decode_block_replays_in_a_graph(T):
+    """Both one-wavefront decoders: 64-chunk blocks and 128-chunk blocks."""
     import torch
     wa = synth.gaussian(3_000_017, 0.02, 81)
     wb = synth.gaussian(1_500_001, 0.03, 82)
-    da = codec.to_device(codec.encode(wa), "cuda")
-    db = codec.to_device(codec.encode(wb), "cuda")
+    lay = codec.make_layout(8, T, 11)
+    da = codec.to_device(codec.encode(wa, layout=lay), "cuda")
+    db = codec.to_device(codec.encode(wb, layout=lay), "cuda")
     out_a = torch.full((wa.size,), 0x5A5A, dtype=torch.int16, device="cuda")
     out_b = torch.empty(wb.size, dtype=torch.int16, device="cuda")
     ref_a = torch.from_numpy(wa.view(np.int16)).cuda()
