@@ -6,7 +6,9 @@
 // per lane, decoded as two interleaved lookup chains) -- the block's prefix
 // sum is then a wave-level DPP scan and no workgroup barrier is needed, so
 // the waves of a CU drift into different phases and decode overlaps memory
-// streaming -- or by one workgroup when T >= 256.  The grid is persistent:
+// streaming -- or, when T >= 256, by one workgroup: T threads with a chunk
+// each (T = 256, 512), or T/2 threads whose waves take 128 of the chunks as
+// lane pairs (T = 1024).  The grid is persistent:
 // decode tables are staged into LDS once per workgroup and shared by all of
 // its waves.
 //
@@ -169,7 +171,75 @@ __global__ __launch_bounds__(64 * W) void df11_decode_pair_kernel(DecodeArgs a) 
     }
 }
 
-// T >= 256: one workgroup of T threads per block.
+// T = 1024: one workgroup of T/2 threads per block, each wave decoding 128
+// chunks as lane pairs like the kernel above.  The waves' counts meet in
+// LDS, every wave ORs its exponents into one block buffer, and the workgroup
+// assembles the block together.  Where LDS holds two block buffers they
+// alternate between blocks: a buffer is cleared while the other is still
+// being assembled, so a block needs two barriers (counts, then exponents).
+// With one buffer, a third barrier waits for the previous block's assembly.
+template <uint32_t T>
+__global__ __launch_bounds__(T / 2) void df11_decode_block_pair_kernel(DecodeArgs a) {
+    constexpr uint32_t NT = T / 2;
+    extern __shared__ __align__(16) uint8_t lds[];
+    const uint32_t tid = threadIdx.x;
+    const uint32_t lane = tid & 63u;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    PairWords pw{};
+    if (blockIdx.x < a.num_blocks) pw = load_pair(a, blockIdx.x, blockIdx.x * T + 2u * tid);
+    stage_table_blob(a, lds, tid, NT);
+    const Tables tb = stage_tables(a, lds);
+    uint32_t *wave_sums = reinterpret_cast<uint32_t *>(lds + a.table_lds_bytes);
+    uint8_t *const buf0 = lds + a.table_lds_bytes + 4 * kScanSlots;
+    const uint32_t cap = a.buf_bytes - 8u;
+    __syncthreads();
+    if (blockIdx.x >= a.num_blocks) return;
+    Chunk A, B;
+    pair_setup(a, pw, blockIdx.x * T + 2u * tid, A, B);
+    Range r = block_range(a, pw.bp0, pw.bp1);
+
+    uint32_t parity = 0;
+    for (uint32_t b = blockIdx.x; b < a.num_blocks; b += gridDim.x) {
+        const uint32_t bn = b + gridDim.x;
+        PairWords nxt = pw;
+        if (bn < a.num_blocks) nxt = load_pair(a, bn, bn * T + 2u * tid);
+        uint2 S[kPrePair];
+        prefetch_sm(a, r, tid, NT, S);
+        const uint32_t edge_sm = prefetch_edge_sm(a, r, tid);
+
+        // with two buffers this one was last read two blocks ago, before the
+        // previous block's barriers
+        if (!a.twin_bufs) __syncthreads();  // the previous block is assembled
+        uint8_t *buf = buf0 + (a.twin_bufs ? parity : 0u) * a.buf_bytes;
+        uint32_t *buf32 = reinterpret_cast<uint32_t *>(buf);
+        for (uint32_t i = tid; i < (a.buf_bytes >> 4); i += NT)
+            reinterpret_cast<uint4 *>(buf)[i] = make_uint4(0u, 0u, 0u, 0u);
+
+        uint32_t syA[kKeepPair], npkA[(kKeepPair + 3) / 4], syB[kKeepPair],
+            npkB[(kKeepPair + 3) / 4], restA, restB, cntA, cntB;
+        decode_count_pair(tb, A, B, syA, npkA, syB, npkB, &restA, &restB, &cntA, &cntB);
+        const uint32_t cnt = cntA + cntB;
+        const uint32_t incl = wave_inclusive_scan(cnt);
+        if (lane == 63u) wave_sums[wave] = incl;
+        __syncthreads();  // every wave's count is in, the buffer is cleared
+        uint32_t before = 0;
+        for (uint32_t w = 0; w < wave; ++w) before += wave_sums[w];
+        const uint32_t off = r.shift + before + incl - cnt;
+        emit_exponents(tb, A, syA, npkA, restA, off, buf32, cap);
+        emit_exponents(tb, B, syB, npkB, restB, off + cntA, buf32, cap);
+        __syncthreads();  // the block's exponents are all in the buffer
+
+        assemble_block(a, r, buf, tid, NT, S, edge_sm);
+        parity ^= 1u;
+        pw = nxt;
+        pair_setup(a, pw, bn * T + 2u * tid, A, B);
+        r = block_range(a, pw.bp0, pw.bp1);
+    }
+}
+
+// T = 256, 512: one workgroup of T threads per block, a chunk per thread.
+// (Two chunks per lane would halve the waves of a workgroup, and the tables
+// staged per workgroup would then cap the waves per CU.)
 template <uint32_t T>
 __global__ __launch_bounds__(T) void df11_decode_block_kernel(DecodeArgs a) {
     extern __shared__ __align__(16) uint8_t lds[];
@@ -223,7 +293,7 @@ using KernelFn = void (*)(DecodeArgs);
 struct LaunchShape {
     uint32_t threads, lut_bits, buf;  // key
     KernelFn fn;
-    uint32_t block, lds, per_cu, waves_per_group;
+    uint32_t block, lds, per_cu, waves_per_group, twin_bufs;
 };
 
 struct DeviceInfo {
@@ -269,7 +339,7 @@ KernelFn block_kernel(uint32_t T, int *slot) {
     switch (T) {
         case 256: *slot = 8; return df11_decode_block_kernel<256>;
         case 512: *slot = 9; return df11_decode_block_kernel<512>;
-        case 1024: *slot = 10; return df11_decode_block_kernel<1024>;
+        case 1024: *slot = 10; return df11_decode_block_pair_kernel<1024>;
         default: return nullptr;
     }
 }
@@ -292,7 +362,8 @@ int fit(DeviceInfo &di, int slot, KernelFn fn, uint32_t threads, uint32_t lds, i
     return DF11_OK;
 }
 
-int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *block, uint32_t *lds) {
+int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *block, uint32_t *lds,
+              uint32_t *twin_bufs) {
     const uint32_t T = s->layout.threads_per_block;
     const uint32_t K = s->layout.lut_bits;
     const uint32_t tab = static_cast<uint32_t>(df11tab::lds_bytes(K));
@@ -312,7 +383,7 @@ int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *bloc
     for (const LaunchShape &ls : di.shapes)
         if (ls.threads == T && ls.lut_bits == K && ls.buf == buf) found = &ls;
     if (!found) {
-        LaunchShape ls{T, K, buf, nullptr, 0, 0, 0, 1};
+        LaunchShape ls{T, K, buf, nullptr, 0, 0, 0, 1, 0};
         if (T == 64 || T == 128) {
             // one wave per block: most resident waves per CU; fewer waves per
             // workgroup on a tie
@@ -333,6 +404,22 @@ int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *bloc
                 }
             }
             if (!best_waves) return DF11_E_UNSUPPORTED;
+        } else if (T == 1024) {
+            int slot = 0, pc = 0;
+            ls.fn = block_kernel(T, &slot);
+            ls.block = T / 2;
+            ls.twin_bufs = 1;
+            ls.lds = tab + 4 * kScanSlots + 2 * buf;  // two block buffers
+            int rc = fit(di, slot, ls.fn, T / 2, ls.lds, &pc);
+            if (rc) return rc;
+            if (pc < 1) {  // one buffer (very compressible streams: large blocks)
+                ls.twin_bufs = 0;
+                ls.lds = tab + 4 * kScanSlots + buf;
+                rc = fit(di, slot, ls.fn, T / 2, ls.lds, &pc);
+                if (rc) return rc;
+            }
+            if (pc < 1) return DF11_E_UNSUPPORTED;
+            ls.per_cu = static_cast<uint32_t>(pc);
         } else {
             int slot = 0, pc = 0;
             ls.fn = block_kernel(T, &slot);
@@ -350,6 +437,7 @@ int shape_for(const df11_stream *s, KernelFn *fn, uint32_t *grid, uint32_t *bloc
     *fn = found->fn;
     *block = found->block;
     *lds = found->lds;
+    *twin_bufs = found->twin_bufs;
     const uint64_t W = found->waves_per_group;
     const uint64_t nb = s->sizes.num_blocks;
     const uint64_t blocks_needed = (nb + W - 1) / W;
@@ -377,7 +465,8 @@ int df11_decode_launch_shape(const df11_stream *s, uint32_t *grid, uint32_t *blo
     if (rc) return rc;
     if (!grid || !block || !lds_bytes) return DF11_E_INVALID_ARG;
     KernelFn fn;
-    return shape_for(s, &fn, grid, block, lds_bytes);
+    uint32_t twin;
+    return shape_for(s, &fn, grid, block, lds_bytes, &twin);
 }
 
 int df11_decode_block(const df11_stream *s, uint16_t *out, hipStream_t stream) {
@@ -386,8 +475,8 @@ int df11_decode_block(const df11_stream *s, uint16_t *out, hipStream_t stream) {
     if (s->sizes.n_elems == 0) return DF11_OK;
     if (!out || (reinterpret_cast<uintptr_t>(out) & 15u)) return DF11_E_INVALID_ARG;
     KernelFn fn;
-    uint32_t grid, block, lds;
-    rc = shape_for(s, &fn, &grid, &block, &lds);
+    uint32_t grid, block, lds, twin;
+    rc = shape_for(s, &fn, &grid, &block, &lds, &twin);
     if (rc) return rc;
     DecodeArgs a;
     a.exp = s->exp;
@@ -404,6 +493,7 @@ int df11_decode_block(const df11_stream *s, uint16_t *out, hipStream_t stream) {
     a.max_len = s->sizes.max_code_len;
     a.table_lds_bytes = static_cast<uint32_t>(df11tab::lds_bytes(s->layout.lut_bits));
     a.buf_bytes = buf_bytes_for(s->sizes.max_elems_per_block);
+    a.twin_bufs = twin;
     hipLaunchKernelGGL(fn, dim3(grid), dim3(block), lds, stream, a);
     return hipGetLastError() == hipSuccess ? DF11_OK : DF11_E_HIP;
 }

@@ -35,6 +35,7 @@ struct DecodeArgs {
     uint32_t max_len;
     uint32_t table_lds_bytes;
     uint32_t buf_bytes;        // exponent buffer, multiple of 16
+    uint32_t twin_bufs;        // T >= 256: two block buffers alternate (else one)
 };
 
 __device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b ? a : b; }

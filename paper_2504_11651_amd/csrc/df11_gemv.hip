@@ -423,6 +423,7 @@ int df11_block_gemv(const df11_stream *dev, const df11_matrix *mats, uint32_t n_
     a.max_len = dev->sizes.max_code_len;
     a.table_lds_bytes = static_cast<uint32_t>(df11tab::lds_bytes(dev->layout.lut_bits));
     a.buf_bytes = buf_bytes_for(dev->sizes.max_elems_per_block);
+    a.twin_bufs = 0;  // not used by the fused kernel
     g.n_mats = n_mats;
     g.part = static_cast<float *>(workspace);
     ReduceArgs ra{};

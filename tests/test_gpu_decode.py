@@ -71,14 +71,19 @@ def test_long_codes_through_escape_path(cap, K):
     assert np.array_equal(got, ref)
 
 
-@pytest.mark.parametrize("T", [64, 128, 256])
+@pytest.mark.parametrize("T", [64, 128, 256, 1024])
 def test_launch_shape(T):
-    """The decoder's launch for a stream long enough to fill the GPU: with
-    T = 64 or 128 one wavefront per block, W = block/64 waves per workgroup
-    sharing the tables, LDS = tables + one output buffer per wave, a
-    persistent grid of whole CUs' worth of workgroups and at least 3 waves
-    per SIMD; with T = 256 one workgroup of T threads per block, LDS = tables
-    + 16 scan slots + one buffer.  The decode in that shape is bit-exact."""
+    """The decoder's launch for a stream long enough to fill the GPU:
+    - T = 64 or 128: one wavefront per block, W = block/64 waves per
+      workgroup sharing the tables, LDS = tables + one output buffer per
+      wave, a persistent grid of whole CUs' worth of workgroups, at least 3
+      waves per SIMD;
+    - T = 256: one workgroup of T threads per block, LDS = tables + 16 scan
+      slots + one block buffer;
+    - T = 1024: one workgroup of T/2 threads (two chunks per lane), LDS =
+      tables + 16 scan slots + two block buffers (one where two do not fit:
+      the one-symbol stream at T = 1024 in test_decode_matches_oracle).
+    The decode in that shape is bit-exact."""
     import torch
     w = synth.gaussian(40_000_000, 0.02, 5)
     hs = codec.encode(w, layout=codec.make_layout(8, T, 11))
@@ -94,6 +99,9 @@ def test_launch_shape(T):
         assert lds == tables + W * buf
         assert grid <= (nb + W - 1) // W and grid % cus == 0
         assert grid * W >= 3 * 4 * cus  # at least 3 waves per SIMD
+    elif T == 1024:
+        assert block == T // 2 and lds == tables + 4 * 16 + 2 * buf
+        assert grid <= nb
     else:
         assert block == T and lds == tables + 4 * 16 + buf
         assert grid <= nb
