@@ -162,10 +162,13 @@ int df11_validate(const df11_stream *host_view);
  * as one stream decodes in one launch (Sec. 2.3.3).  The work is enqueued
  * on `stream` and the call returns without waiting; buffers must stay alive
  * until the stream has executed it.  n_elems == 0 launches nothing.
- * Returns DF11_E_UNSUPPORTED for bytes_per_thread != 8, DF11_E_INVALID_ARG for
- * a null or misaligned pointer (exp 8-byte, sm and tables 16-byte, gaps and
- * block_pos 4-byte aligned) or inconsistent sizes, DF11_E_HIP when the launch
- * fails. */
+ * T = 64 and 128 decode one block per wavefront (T = 128 with two chunks
+ * per lane), T = 256, 512 and 1024 one block per workgroup.
+ * Returns DF11_E_UNSUPPORTED for bytes_per_thread != 8, for threads_per_block
+ * outside {64, 128, 256, 512, 1024}, or when no workgroup of the launch fits
+ * the device's LDS; DF11_E_INVALID_ARG for a null or misaligned pointer (exp
+ * 8-byte, sm and tables 16-byte, gaps and block_pos 4-byte aligned) or
+ * inconsistent sizes; DF11_E_HIP when the launch fails. */
 int df11_decode_block(const df11_stream *dev, uint16_t *out, hipStream_t stream);
 
 /* Launch shape df11_decode_block would use on the current device for this
