@@ -8,13 +8,15 @@
 // loads, and keeps several kilobytes in flight per wave:
 //   - one wavefront computes a tile of 16 output features x all tokens over a
 //     contiguous range of k; all matrices of the block share one launch;
-//   - per 64 k a lane loads 2 x 8 BF16 of one weight row (lanes 16g..16g+15
-//     take rows 0..15 at k offset 16g) and the matching activations, and
-//     issues v_mfma_f32_16x16x32_bf16 twice per 16-token slice; A (tokens)
-//     and B (features) use the same assignment of k to lanes, so the dot
-//     products cover each k once whatever order the unit sums in;
-//   - up to 3 tokens each wave reads its activations from memory; from 4,
-//     a workgroup of 4 waves stages each 256-k activation slab in LDS once;
+//   - per 64 k a lane feeds 2 x 8 BF16 of one weight row (lanes 16g..16g+15
+//     take rows 0..15 at k offset 16g) and the matching activations to
+//     v_mfma_f32_16x16x32_bf16, twice per 16-token slice; A (tokens) and B
+//     (features) use the same assignment of k to lanes, so the dot products
+//     cover each k once whatever order the unit sums in;
+//   - up to 3 tokens each wave loads its weights straight into that layout
+//     and reads its activations from memory; from 4, a workgroup of 4 waves
+//     stages each 256-k activation slab in LDS once, and each wave passes
+//     its weights through LDS so that every load reads whole cache lines;
 //   - a matrix is split into k ranges of about 1024 columns (up to 32
 //     tokens) or 4096 columns, or half that where it evens out the work per
 //     CU (more tokens); each range of a split matrix writes fp32 partial
@@ -197,16 +199,30 @@ __global__ __launch_bounds__(64 * kWaves) void gemm_tiles_kernel(GemmArgs a) {
 // Four or more tokens: a workgroup of kSlabWaves waves covers 16*kSlabWaves features
 // over one k range and stages the activations of each 256-k slab in LDS once
 // for all its waves (rows padded by 16 bytes so the 16 lanes of one read
-// pass hit distinct banks).  Weights still stream straight into registers.
+// pass hit distinct banks).
+// Each wave's weights pass through 8 KB of LDS of its own: a load
+// instruction reads 512 contiguous bytes of each of two rows (8 whole cache
+// lines) rather than 64 bytes of each of 16 rows, which streams the
+// 4096-column matrices about a tenth faster; written with row r's 16-byte
+// piece p at slot (p + r) mod 32, the slab is read back in the matrix-core
+// layout without bank conflicts.  Only the wave that writes a weight slab
+// reads it, and one wave's LDS accesses complete in order, so the weights
+// need no barrier.
 constexpr uint32_t kSlabK = kKPerIter;              // k per staged slab
 constexpr uint32_t kSlabStride = kSlabK * 2 + 16;   // bytes per token row in LDS
+constexpr uint32_t kWaveW = kTileRows * kSlabK * 2; // bytes of one wave's weight slab
 
-// (4 waves per SIMD: the accumulators then stay in VGPRs, which the compiler
-// otherwise spills to AGPRs at 3 waves per SIMD)
+// LDS of one workgroup, and the waves per SIMD it leaves room for (at most
+// 4): the register hint asks for exactly that many
 template <uint32_t MT>
-__global__ __launch_bounds__(64 * kSlabWaves) __attribute__((amdgpu_waves_per_eu(4))) void
+constexpr uint32_t kSlabLds = 16 * MT * kSlabStride + kSlabWaves * kWaveW;
+template <uint32_t MT>
+constexpr uint32_t kSlabOcc = 160u * 1024u / kSlabLds<MT> < 4u ? 160u * 1024u / kSlabLds<MT> : 4u;
+
+template <uint32_t MT>
+__global__ __launch_bounds__(64 * kSlabWaves) __attribute__((amdgpu_waves_per_eu(kSlabOcc<MT>))) void
 gemm_slab_kernel(GemmArgs a) {
-    __shared__ __attribute__((aligned(16))) uint8_t slab[16 * MT * kSlabStride];
+    __shared__ __attribute__((aligned(16))) uint8_t slab[kSlabLds<MT>];
     const uint32_t tid = threadIdx.x;
     const uint32_t lane = tid & 63u;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -223,8 +239,6 @@ gemm_slab_kernel(GemmArgs a) {
 
     const uint32_t j = lane & 15u;
     const uint32_t g = lane >> 4;
-    const uint16_t *wrow =
-        a.w + m.w_off + static_cast<uint64_t>(active ? rb * kTileRows + j : 0u) * m.cols + 8u * g;
 
     // slab loading: 16-byte piece q = tid + 64*kSlabWaves*i covers token
     // q / kRowPieces, k offset 8 * (q % kRowPieces) of the slab
@@ -262,14 +276,23 @@ gemm_slab_kernel(GemmArgs a) {
                 masked(xr[i], ok ? ~0u : 0u);
         }
     };
-    // weights of 64-k step u of the slab at k (steps past the range repeat
-    // its last step: in bounds, and not used)
-    uint4 W[kUnroll][2];
-    auto load_w = [&](uint32_t u, uint32_t k) {
-        const uint32_t steps = umin(kUnroll, (k1 - k) / kKStep);
-        const uint32_t kk = k + kKStep * umin(u, steps - 1u);
-        W[u][0] = load16(wrow + kk);
-        W[u][1] = load16(wrow + kk + 32u);
+    // weights: load i of a slab reads rows 2i and 2i+1 of the tile (lane:
+    // row 2i + lane/32, 16-byte piece lane%32 of the slab; pieces past the
+    // range repeat its last piece).  A plain vector type keeps the eight
+    // registers out of private memory.
+    typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+    u32x4v W[8];
+    u32x4v *wl = reinterpret_cast<u32x4v *>(slab + 16 * MT * kSlabStride + wave * kWaveW);
+    const uint32_t half = lane >> 5, pl = lane & 31u;
+    const uint16_t *wrow2 =
+        a.w + m.w_off + static_cast<uint64_t>(active ? rb * kTileRows + half : 0u) * m.cols;
+    auto load_w = [&](uint32_t i, uint32_t k) {
+        const uint32_t p = umin(pl, umin(32u, (k1 - k) / 8u) - 1u);
+        W[i] = *reinterpret_cast<const u32x4v *>(wrow2 + static_cast<uint64_t>(2u * i) * m.cols + k + 8u * p);
+    };
+    auto put_w = [&](uint32_t i) {
+        const uint32_t r = 2u * i + half;
+        wl[r * 32u + ((pl + r) & 31u)] = W[i];
     };
     f32x4 acc[MT];
 #pragma unroll
@@ -280,15 +303,17 @@ gemm_slab_kernel(GemmArgs a) {
             const uint8_t *row = slab + (16u * mt + j) * kSlabStride + 2u * (kKStep * u + 8u * g);
             const uint4 x0 = *reinterpret_cast<const uint4 *>(row);
             const uint4 x1 = *reinterpret_cast<const uint4 *>(row + 64u);
-            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x0), as_bf16x8(W[u][0]),
+            const u32x4v w0 = wl[j * 32u + ((8u * u + g + j) & 31u)];
+            const u32x4v w1 = wl[j * 32u + ((8u * u + 4u + g + j) & 31u)];
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x0), __builtin_bit_cast(bf16x8, w0),
                                                               acc[mt], 0, 0, 0);
-            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x1), as_bf16x8(W[u][1]),
+            acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(x1), __builtin_bit_cast(bf16x8, w1),
                                                               acc[mt], 0, 0, 0);
         }
     };
 
 #pragma unroll
-    for (uint32_t u = 0; u < kUnroll; ++u) load_w(u, k0);
+    for (uint32_t i = 0; i < 8; ++i) load_w(i, k0);
     load_slab(k0);
     store_slab(k0);
     __syncthreads();
@@ -296,20 +321,27 @@ gemm_slab_kernel(GemmArgs a) {
     for (; k + kSlabK < k1; k += kSlabK) {
         const uint32_t kn = k + kSlabK;
         load_slab(kn);
-        // each step's weight registers take the next slab's weights as soon
-        // as its products are issued: a wave keeps kUnroll steps of weights
-        // in flight across the barriers
+        // each weight register takes the next slab's load as soon as it is
+        // in LDS (kept in this order: hoisting the loads would make the
+        // compiler copy registers, and each copy waits for its load)
 #pragma unroll
-        for (uint32_t u = 0; u < kUnroll; ++u) {
-            if (active) products(u);
-            load_w(u, kn);
+        for (uint32_t i = 0; i < 8; ++i) {
+            put_w(i);
+            __builtin_amdgcn_sched_barrier(0);
+            load_w(i, kn);
+            __builtin_amdgcn_sched_barrier(0);
         }
+#pragma unroll
+        for (uint32_t u = 0; u < kUnroll; ++u)
+            if (active) products(u);
         __syncthreads();  // every wave is done with this slab
         store_slab(kn);
         __syncthreads();
     }
     // the last slab of the range
     const uint32_t steps = umin(kUnroll, (k1 - k) / kKStep);  // uniform
+#pragma unroll
+    for (uint32_t i = 0; i < 8; ++i) put_w(i);
 #pragma unroll
     for (uint32_t u = 0; u < kUnroll; ++u)
         if (active && u < steps) products(u);
