@@ -196,7 +196,7 @@ typedef struct {
 
 /* Device workspace bytes df11_block_gemm / df11_block_forward need for these
  * matrices at this many tokens: room for the fp32 partial sums of the
- * matrices whose cols are split into k ranges (0 when none is).  Above 32
+ * matrices whose cols are split into k ranges (0 when none is).  Above 8
  * tokens the split is chosen per device to balance its compute units; the
  * value covers every choice, so it depends only on the shapes.  Host, no
  * device access. */
@@ -246,7 +246,7 @@ int df11_block_forward(const df11_stream *dev, uint16_t *weights_out, const df11
  *   returns DF11_E_BUFFER_TOO_SMALL when these matrices at this many tokens
  *   need more partial sums than the array holds (df11_gemm_workspace_bytes
  *   > DF11_STATIC_SCRATCH_BYTES): the Llama-3-8B block shapes fit at every
- *   token count up to DF11_MAX_TOKENS, the Llama-3.1-70B block up to 10;
+ *   token count up to DF11_MAX_TOKENS, the Llama-3.1-70B block up to 20;
  *   otherwise the same arguments, checks and results as df11_block_forward
  *   (bit-identical outputs).
  * All calls on one GPU share its array: calls that overlap in time on one

@@ -17,7 +17,7 @@
 //     and reads its activations from memory; from 4, a workgroup of 4 waves
 //     stages each 256-k activation slab in LDS once, and each wave passes
 //     its weights through LDS so that every load reads whole cache lines;
-//   - a matrix is split into k ranges of about 1024 columns (up to 32
+//   - a matrix is split into k ranges of about 1024 columns (up to 8
 //     tokens) or 4096 columns, or half that where it evens out the work per
 //     CU (more tokens); each range of a split matrix writes fp32 partial
 //     sums, and a second kernel adds them in a fixed order, so results are
@@ -40,12 +40,12 @@ constexpr uint32_t kKStep = 64;      // k per inner step: two MFMAs
 constexpr uint32_t kUnroll = 4;      // inner steps whose weight loads are issued together
 constexpr uint32_t kKPerIter = kKStep * kUnroll;
 // k range of one wave before a matrix is split: short ranges (more
-// workgroups in flight) pay off while the products are light; from 33
-// tokens the products per weight favour long ranges, and the split is
-// chosen to balance the CUs
+// workgroups in flight) pay off while the products are light; from 9
+// tokens the products per weight favour long ranges (whose weights pass
+// through LDS), and the split is chosen to balance the CUs
 constexpr uint32_t kKTargetFew = 1024;
 constexpr uint32_t kKTargetMany = 4096;
-constexpr uint32_t kFewTokens = 32;
+constexpr uint32_t kFewTokens = 8;
 constexpr uint32_t kSlabMinTokens = 4;  // fewer tokens: activations straight from memory
 constexpr uint32_t kWaves = 4;       // waves per workgroup, up to 3 tokens
 constexpr uint32_t kSlabWaves = 4;   // waves per workgroup sharing one activation slab

@@ -17,18 +17,18 @@ def llama_mats():
 
 
 def test_workspace_closed_form():
-    # up to 32 tokens every matrix is split into k ranges of 1024 columns
+    # up to 8 tokens every matrix is split into k ranges of 1024 columns
     # (4 for the 4096-column matrices, 14 for down); partial sums of rows x
     # ranges x tokens floats
     mats, _ = llama_mats()
     few = 4 * (4096 + 1024 + 1024 + 4096 + 14336 + 14336) + 14 * 4096
-    for t in (1, 7, 16, 32):
+    for t in (1, 7, 8):
         assert codec.gemm_workspace_bytes(mats, t) == 4 * few * t
-    # from 33 tokens the base ranges are 4096 columns (1 per 4096-column
+    # from 9 tokens the base ranges are 4096 columns (1 per 4096-column
     # matrix, 4 for down) and a device may double any matrix's ranges to
     # balance its CUs: the workspace covers the doubled split of every matrix
     many = 2 * (4096 + 1024 + 1024 + 4096 + 14336 + 14336) + 8 * 4096
-    for t in (33, 64):
+    for t in (9, 16, 33, 64):
         assert codec.gemm_workspace_bytes(mats, t) == 4 * many * t
     assert codec.gemm_workspace_bytes([(0, 16, 1024)], 5) == 0
     assert codec.gemm_workspace_bytes([(0, 16, 256)], 40) == 0

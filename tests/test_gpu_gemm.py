@@ -58,10 +58,10 @@ SHAPES = [
     [(48, 320)],
     [(32, 4096)],
     [(16, 4160)],               # k ranges ending in a 64-wide partial slab
-    [(64, 8192)],               # split into 8 (up to 32 tokens) or 2 k ranges
+    [(64, 8192)],               # split into 8 (up to 8 tokens) or 2 k ranges
     [(64, 256), (16, 256), (16, 256), (64, 256), (128, 256), (128, 256), (64, 4352)],
 ]
-TOKENS = [1, 2, 3, 4, 15, 16, 17, 32, 33, 48, 64]
+TOKENS = [1, 2, 3, 4, 8, 9, 15, 16, 17, 32, 33, 48, 64]
 
 
 @pytest.mark.parametrize("si", range(len(SHAPES)))
