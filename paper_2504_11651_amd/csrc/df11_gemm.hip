@@ -246,11 +246,12 @@ gemm_slab_kernel(GemmArgs a) {
     constexpr uint32_t kPieces = 16u * MT * kRowPieces;
     constexpr uint32_t kPer = kPieces / (64u * kSlabWaves);
     static_assert(kPieces % (64u * kSlabWaves) == 0, "whole pieces per thread");
-    // Inside the loop every slab has a next one, whose activations and
-    // weights are all requested before this slab's products wait for
-    // anything; loads complete in order, so the wait for one load never
-    // waits for loads issued after it.  Activations are masked when staged,
-    // not when they arrive (a use on arrival would wait for every older load).
+    // Inside the loop every slab has a next one: its activations are
+    // requested first, and each weight register's next load right after the
+    // register is written to LDS, so a slab of weights stays in flight;
+    // loads complete in order, so the wait for one load never waits for
+    // loads issued after it.  Activations are masked when staged, not when
+    // they arrive (a use on arrival would wait for every older load).
     uint4 xr[kPer];
     auto slab_piece = [&](uint32_t i, uint32_t k, uint32_t *t, uint32_t *kk) {
         const uint32_t q = tid + 64u * kSlabWaves * i;
